@@ -1,0 +1,246 @@
+"""CPU oracle for group-wise signed symmetric quantization and its dequantizing matmul.
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke check in
+``__graft_entry__`` and the ``cpu_baseline`` leg of ``bench.py`` may import this
+module.  It shares no code with the HIP library (``paper_2607_08779_amd``) and
+imports nothing from it: every function here takes plain numpy arrays.
+
+The oracle is written to be read against the paper (Colbert, Dash et al.,
+"Signed Symmetric Quantization for Few-Bit Integers"):
+
+* Sec. 1, Eq. (1): the standard integer quantizer
+  Q(w) = s * (clip(round(w/s + z); A_q) - z).
+* Sec. 3, Eq. (2): the min-max asymmetric grid on the unsigned alphabet.
+* Sec. 3, Eq. (3): the absmax ("unsigned symmetric") grid, s = ||w||_inf / 2^(q-1) > 0.
+* Sec. 3, Eq. (4)-(5): the signed symmetric family s = gamma*alpha and the sign
+  rule gamma* = -sign(w_{i*}), i* = argmax |w_i|.
+* App. B.1 (formats table): one fp16 scale per 32-weight block, packed few-bit
+  indices, no zero point for the symmetric formats.
+* App. B.3 (zero-point cost): Y_ik = sum_b s_kb sum_{j in b} X_ij (Wq_kj - z_kb).
+
+Arithmetic precision.  The paper fixes no precision for the grid computation;
+this oracle computes the scale and the quotient w/s in IEEE binary32 (each
+operation correctly rounded, round-half-to-even everywhere), stores the scale
+as IEEE binary16 (round-half-to-even) and evaluates the matmul in binary64.
+The readings taken where the paper is silent are listed in ``READINGS`` and
+each is cited at the line that implements it.
+
+Parity status: every public function here is pinned by tests/test_oracle_pins.py
+against closed forms, the paper's theorems (Lemma 1, Theorem 1, Corollary 1,
+Theorem 2), brute force over the alphabet and a library quantizer
+(``torch.fake_quantize_per_tensor_affine``).  No function is "parity unpinned".
+"""
+from __future__ import annotations
+
+from typing import NamedTuple, Optional
+
+import numpy as np
+
+SIGNED_SYM = 0      # signed absmax grid, Eq. (5)
+UNSIGNED_SYM = 1    # absmax grid with s > 0, Eq. (3)
+ASYM = 2            # min-max grid with an integer zero point, Eq. (2)
+
+MODE_NAMES = {SIGNED_SYM: "signed_sym", UNSIGNED_SYM: "unsigned_sym", ASYM: "asym"}
+
+READINGS = {
+    "tie_break": "Eq. (5) asks for deterministic tie-breaking in argmax|w_i|; when both +M and -M "
+                 "occur the oracle takes gamma=+1 (gamma=-1 only if max(w) > -min(w) strictly).",
+    "rounding": "The round-to-nearest operator of Eq. (1) resolves exact halves to even.",
+    "division": "t = w/s is one IEEE binary32 division, correctly rounded, then rounded to an integer.",
+    "scale_storage": "Codes are computed from the binary32 scale; the stored scale is its binary16 "
+                     "rounding (half to even).",
+    "amax_zero": "Sec. 4 assumes M > 0; for an all-zero group the oracle stores scale +0 and code 0.",
+    "asym_zero_point": "Eq. (2) gives a real z = -min/s; with an unsigned integer zero point the "
+                       "range is first widened to contain 0 (min' = min(min w, 0), max' = "
+                       "max(max w, 0)), so z = rne(fl32(-min'/s)) lies in [0, 2^q-1] and the grid "
+                       "still covers the data.  Codes are clip(rne(fl32(w/s)) + z, 0, 2^q-1), the "
+                       "zero point being added after rounding; an all-zero group stores zeros.",
+    "index_encoding": "Symmetric codes c in A_q are stored as the offset-binary index u = c + 2^(q-1).",
+    "bit_order": "Field k of a row occupies bits [k*q, k*q+q) of the row's little-endian bit stream.",
+}
+
+
+class Quantized(NamedTuple):
+    """Result of :func:`quantize` (all arrays row-major)."""
+
+    codes: np.ndarray                 # uint8 [rows, cols*q/8], packed indices
+    scales: np.ndarray                # uint16 [rows, cols/group], binary16 bit patterns
+    zp: Optional[np.ndarray]          # uint8 [rows, cols/group] for ASYM, else None
+    scale32: np.ndarray               # float32 [rows, cols/group], the scale the codes used
+    u: np.ndarray                     # int64 [rows, cols], unpacked indices
+
+
+# ---------------------------------------------------------------------------
+# Exact conversions between storage formats and binary32/binary64.
+# ---------------------------------------------------------------------------
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Widen bfloat16 bit patterns to binary32 exactly (bf16 is the top half of binary32)."""
+    b = np.ascontiguousarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return b.view(np.float32)
+
+
+def f16_bits_from_f32(x: np.ndarray) -> np.ndarray:
+    """Round binary32 values to binary16 (IEEE, half to even) and return the bit patterns."""
+    return np.asarray(x, dtype=np.float32).astype(np.float16).view(np.uint16)
+
+
+def f16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Exact value of binary16 bit patterns as binary64."""
+    return np.ascontiguousarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Eq. (1): the standard integer quantizer, evaluated in binary32.
+# ---------------------------------------------------------------------------
+
+def eq1_codes(w: np.ndarray, s: np.ndarray, z: np.ndarray, lo: int, hi: int) -> np.ndarray:
+    """Integer part of Eq. (1): clip(round(w/s) + z; [lo, hi]) for an integer zero point z.
+
+    w/s is one correctly rounded binary32 division, rounding is half-to-even
+    (numpy.rint) and, because z is an integer, round(w/s + z) = round(w/s) + z.
+    Returns the clipped integers as float32 (exact).
+    """
+    w = np.asarray(w, dtype=np.float32)
+    s = np.asarray(s, dtype=np.float32)
+    t = w / s                                       # binary32, correctly rounded
+    r = np.rint(t) + np.asarray(z, dtype=np.float32)
+    return np.clip(r, np.float32(lo), np.float32(hi))
+
+
+def signed_alphabet(q: int) -> tuple[int, int]:
+    """A_q = {-2^(q-1), ..., 2^(q-1)-1} (Sec. 1 notation; Sec. 3, Eq. (3))."""
+    return -(1 << (q - 1)), (1 << (q - 1)) - 1
+
+
+def unsigned_alphabet(q: int) -> tuple[int, int]:
+    """A_q = {0, ..., 2^q - 1}, the alphabet of the min-max grid (Sec. 3, Eq. (2))."""
+    return 0, (1 << q) - 1
+
+
+# ---------------------------------------------------------------------------
+# Group-wise grids: Eq. (2), Eq. (3), Eq. (4)-(5).
+# ---------------------------------------------------------------------------
+
+def _check_shape(W: np.ndarray, group: int, q: int) -> None:
+    if W.ndim != 2:
+        raise ValueError("W must be 2-D [rows, cols]")
+    if group < 1 or W.shape[1] % group:
+        raise ValueError("cols must be a multiple of group")
+    if not 2 <= q <= 8:
+        raise ValueError("q must be in [2, 8]")
+    if (W.shape[1] * q) % 8:
+        raise ValueError("cols*q must be a multiple of 8 (whole bytes per row)")
+
+
+def quantize(W: np.ndarray, group: int, q: int, mode: int) -> Quantized:
+    """Quantize each group of ``group`` consecutive entries of every row of W.
+
+    W is binary32 [rows, cols] (bf16 inputs are widened exactly first).  Groups run
+    along the reduction index, as in App. B.3.
+    """
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    _check_shape(W, group, q)
+    rows, cols = W.shape
+    G = W.reshape(rows, cols // group, group)
+    mx = G.max(axis=-1)                             # max_j w_j
+    mn = G.min(axis=-1)                             # min_j w_j
+
+    if mode in (SIGNED_SYM, UNSIGNED_SYM):
+        lo, hi = signed_alphabet(q)
+        amax = np.maximum(mx, -mn)                  # M = ||w||_inf  (Eq. (3), Eq. (5))
+        if mode == SIGNED_SYM:
+            # Eq. (5): gamma* = -sign(w_{i*}).  A unique positive extreme gives gamma=-1,
+            # a unique negative extreme gives gamma=+1; a tie +M/-M takes gamma=+1.
+            gamma = np.where(mx > -mn, np.float32(-1), np.float32(1))
+        else:
+            gamma = np.ones_like(amax)              # Eq. (3): s > 0 by convention
+        alpha = np.ldexp(amax, -(q - 1)).astype(np.float32)     # alpha = M / 2^(q-1), exact
+        s32 = (gamma * alpha).astype(np.float32)                # Eq. (4): s = gamma*alpha
+        zero = amax == 0
+        safe_s = np.where(zero, np.float32(1), s32)
+        c = eq1_codes(G, safe_s[..., None], np.float32(0), lo, hi)   # Eq. (1) with z = 0
+        c = np.where(zero[..., None], np.float32(0), c)
+        s32 = np.where(zero, np.float32(0), s32)    # M = 0: scale +0, every code 0
+        u = (c.astype(np.int64) - lo).reshape(rows, cols)   # offset-binary index
+        zp = None
+    elif mode == ASYM:
+        lo, hi = unsigned_alphabet(q)
+        mx0 = np.maximum(mx, np.float32(0))                     # range widened to contain 0 so the
+        mn0 = np.minimum(mn, np.float32(0))                     # integer zero point fits A_q
+        rng32 = (mx0 - mn0).astype(np.float32)                  # fl32(max' - min')
+        s32 = (rng32 / np.float32(hi)).astype(np.float32)       # Eq. (2): s = (max-min)/(2^q-1)
+        flat = s32 == 0                                         # all-zero group
+        safe_s = np.where(flat, np.float32(1), s32)
+        z = np.clip(np.rint(-mn0 / safe_s), np.float32(lo), np.float32(hi))  # Eq. (2): z = -min/s
+        c = eq1_codes(G, safe_s[..., None], z[..., None], lo, hi)    # clip(round(w/s) + z)
+        c = np.where(flat[..., None], np.float32(0), c)
+        z = np.where(flat, np.float32(0), z)
+        u = c.astype(np.int64).reshape(rows, cols)
+        zp = z.astype(np.uint8)
+    else:
+        raise ValueError(f"unknown mode {mode}")
+
+    return Quantized(codes=pack(u, q), scales=f16_bits_from_f32(s32), zp=zp,
+                     scale32=s32.astype(np.float32), u=u)
+
+
+# ---------------------------------------------------------------------------
+# App. B.1: packing q-bit indices, several per byte.
+# ---------------------------------------------------------------------------
+
+def pack(u: np.ndarray, q: int) -> np.ndarray:
+    """Pack indices u in [0, 2^q) into a little-endian bit stream per row.
+
+    Field k of a row occupies stream bits [k*q, k*q+q); stream bit b is bit b%8
+    of byte b//8.  For q=4 this is byte j = u[2j] | u[2j+1] << 4; for q=2 four
+    fields share a byte; for q=3 fields straddle bytes.
+    """
+    u = np.asarray(u, dtype=np.int64)
+    rows, cols = u.shape
+    if (cols * q) % 8:
+        raise ValueError("cols*q must be a multiple of 8")
+    if u.size and (u.min() < 0 or u.max() >= (1 << q)):
+        raise ValueError("index out of range")
+    bits = ((u[..., None] >> np.arange(q)) & 1).astype(np.uint8)     # [rows, cols, q], LSB first
+    return np.packbits(bits.reshape(rows, cols * q), axis=1, bitorder="little")
+
+
+def unpack(codes: np.ndarray, cols: int, q: int) -> np.ndarray:
+    """Inverse of :func:`pack`: int64 indices [rows, cols]."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    rows = codes.shape[0]
+    bits = np.unpackbits(codes, axis=1, bitorder="little")[:, : cols * q]
+    bits = bits.reshape(rows, cols, q).astype(np.int64)
+    return (bits << np.arange(q)).sum(axis=-1)
+
+
+# ---------------------------------------------------------------------------
+# Dequantization and the weight-only matmul (App. B.3).
+# ---------------------------------------------------------------------------
+
+def dequantize(codes: np.ndarray, scales: np.ndarray, zp: Optional[np.ndarray],
+               cols: int, group: int, q: int) -> np.ndarray:
+    """W_hat[n, k] = s[n, b] * (u[n, k] - o[n, b]) in binary64, b = k // group.
+
+    o = 2^(q-1) for the symmetric formats (the index offset) and o = zp for the
+    asymmetric one, i.e. Eq. (1) read back with the stored binary16 scale.
+    """
+    u = unpack(codes, cols, q).astype(np.float64)
+    rows = u.shape[0]
+    s = f16_bits_to_f64(scales).reshape(rows, cols // group, 1)
+    if zp is None:
+        o = np.float64(1 << (q - 1))
+    else:
+        o = np.asarray(zp, dtype=np.float64).reshape(rows, cols // group, 1)
+    return (s * (u.reshape(rows, cols // group, group) - o)).reshape(rows, cols)
+
+
+def matmul(x: np.ndarray, codes: np.ndarray, scales: np.ndarray, zp: Optional[np.ndarray],
+           N: int, K: int, group: int, q: int) -> np.ndarray:
+    """y[m, n] = sum_k x[m, k] * W_hat[n, k], evaluated in binary64 (App. B.3)."""
+    x64 = np.asarray(x, dtype=np.float64).reshape(-1, K)
+    W_hat = dequantize(codes, scales, zp, K, group, q)
+    if W_hat.shape[0] != N:
+        raise ValueError("codes do not have N rows")
+    return x64 @ W_hat.T
