@@ -1,0 +1,268 @@
+"""Benchmark of the signed-symmetric W4 path on one MI355X.
+
+One step is one pass of the whole path over one batch of synthetic input, on
+the Llama3-8B down-projection shape (N=4096 outputs, K=14336, q=4, g=32,
+signed symmetric scales):
+
+  1. quantize the bf16 weight matrix (load, per-group absmax + sign, scale,
+     round/clip, pack)                                   -> ssq_quantize
+  2. decode: one GEMV (M=1) through each of ``--layers`` distinct quantized
+     copies of that matrix, like one token through a stack of layers
+                                                         -> ssq_matmul, M=1
+  3. prefill: a GEMM with M=512 tokens through ``--gemm-layers`` of the copies
+                                                         -> ssq_matmul, M=512
+
+The layer copies total more than the 256 MB Infinity Cache, so the GEMV
+streams its codes from HBM.  Each phase is bracketed by HIP events on the
+stream its kernels run on; a kernel's average duration is the phase time over
+its launches.  ``value`` is the decode GEMV's algorithmic HBM bandwidth (codes
++ scales + x + y bytes per launch over its average duration); the GEMM's
+TFLOP/s and the quantize kernel's bandwidth are reported beside it.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "W4 signed-sym decode GEMV HBM GB/s (% peak) + prefill GEMM TFLOP/s, 4096x14336"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, vendor figure
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_counters.json")
+CSRC = os.path.join(ROOT, "paper_2607_08779_amd", "csrc")
+
+
+def kernel_source_sha(files) -> str:
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+KERNEL_SOURCES = {
+    "gemv": ["gemv.hip", "ssq_internal.h"],
+    "gemm": ["gemm.hip", "ssq_internal.h"],
+    "quantize": ["quantize.hip", "ssq_internal.h"],
+}
+
+
+def measured_traffic(kind: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None if absent
+    or taken on a different version of the kernel's source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            data = json.load(f)
+    except (OSError, ValueError):
+        return None
+    entry = data.get(kind)
+    if not entry or entry.get("source_sha") != kernel_source_sha(KERNEL_SOURCES[kind]):
+        return None
+    return entry.get("hbm_bytes_per_launch")
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--layers", type=int, default=16, help="distinct quantized copies (decode depth)")
+    p.add_argument("--gemm-layers", type=int, default=4, help="prefill GEMMs per step")
+    p.add_argument("--gemm-m", type=int, default=512)
+    p.add_argument("--mode", choices=["signed_sym", "unsigned_sym", "asym"], default="signed_sym")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--phases", default="quantize,gemv,gemm",
+                   help="comma list of phases to run (profiling runs isolate one kernel)")
+    return p.parse_args()
+
+
+def cpu_baseline(w_bits: np.ndarray, x_bits: np.ndarray, N: int, K: int, g: int, q: int,
+                 mode: int, gemv_bytes_per_row: float, budget_s: float = 12.0) -> dict:
+    """Time the CPU oracle (single thread) on a bounded row sample of the same workload."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import ssq_oracle as O
+
+    rows = 512
+    wf_sample = w_bits[:rows]
+    xf = O.bf16_bits_to_f32(x_bits)
+    t_quant = t_gemv = 0.0
+    reps = 0
+    with threadpool_limits(limits=1):
+        t_start = time.perf_counter()
+        while reps < 1 or (time.perf_counter() - t_start < budget_s and reps < 5):
+            t0 = time.perf_counter()
+            r = O.quantize(O.bf16_bits_to_f32(wf_sample), g, q, mode)
+            t1 = time.perf_counter()
+            O.matmul(xf, r.codes, r.scales, r.zp, rows, K, g, q)
+            t2 = time.perf_counter()
+            t_quant += t1 - t0
+            t_gemv += t2 - t1
+            reps += 1
+    gemv_bytes = gemv_bytes_per_row * rows
+    quant_bytes = rows * K * (2 + q / 8 + 2 / g + (1 / g if mode == 2 else 0))
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {
+        "value": round(gemv_bytes * reps / t_gemv / 1e9, 6),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"oracle quantize + binary64 GEMV on rows 0..{rows - 1} of the {N}x{K} matrix "
+                   f"({rows}/{N} of the workload), {reps} repetition(s), one thread"),
+        "quantize_gbs": round(quant_bytes * reps / t_quant / 1e9, 6),
+        "seconds": round(t_quant + t_gemv, 2),
+        "host_cpu": cpu_model,
+        "host_threads_available": os.cpu_count(),
+    }
+
+
+def main() -> int:
+    args = parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        return 2
+    import torch
+
+    from paper_2607_08779_amd import ssq, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    mode = ssq.MODES[args.mode]
+    phases = set(args.phases.split(","))
+
+    wl = synth.llama3_8b_decode()
+    spec = wl.layers["down_proj"]
+    N, K, q, g = spec.rows, spec.cols, 4, 32
+    w_bits = synth.weights(spec)                                   # bf16 bits, host
+    x1_bits = synth.activations(1, K, seed=wl.x_seed)
+    xm_bits = synth.activations(args.gemm_m, K, seed=wl.x_seed + args.gemm_m)
+
+    def dev_bf16(a):
+        return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    W = dev_bf16(w_bits)
+    x1, xm = dev_bf16(x1_bits), dev_bf16(xm_bits)
+    zp_on = mode == ssq.ASYM
+    layers = []
+    for _ in range(args.layers):
+        layers.append(ssq.ssq_quantize(W, g, q, mode))
+    staging = ssq.ssq_quantize(W, g, q, mode)                      # quantize target each step
+    y1 = torch.empty((1, N), dtype=torch.bfloat16, device=dev)
+    ym = torch.empty((args.gemm_m, N), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        if ev:
+            ev[0].record()
+        if "quantize" in phases:
+            ssq.ssq_quantize(W, g, q, mode, out=staging)
+        if ev:
+            ev[1].record()
+        if "gemv" in phases:
+            for r in range(args.layers):
+                c, s, z = layers[(i + r) % args.layers]
+                ssq.ssq_matmul(x1, c, s, z, N, K, g, q, out=y1)
+        if ev:
+            ev[2].record()
+        if "gemm" in phases:
+            for r in range(args.gemm_layers):
+                c, s, z = layers[(i * args.gemm_layers + r) % args.layers]
+                ssq.ssq_matmul(xm, c, s, z, N, K, g, q, out=ym)
+        if ev:
+            ev[3].record()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i, events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    t_q = sum(e[0].elapsed_time(e[1]) for e in events) / 1e3   # seconds
+    t_v = sum(e[1].elapsed_time(e[2]) for e in events) / 1e3
+    t_m = sum(e[2].elapsed_time(e[3]) for e in events) / 1e3
+    t_step = sum(e[0].elapsed_time(e[3]) for e in events) / 1e3 / args.steps
+
+    zp_bytes = N * K // g if zp_on else 0
+    gemv_bytes = N * K * q // 8 + 2 * N * K // g + zp_bytes + 2 * K + 2 * N
+    quant_bytes = 2 * N * K + N * K * q // 8 + 2 * N * K // g + zp_bytes
+    gemm_flops = 2 * args.gemm_m * N * K
+    n_gemv = args.steps * args.layers
+    n_gemm = args.steps * args.gemm_layers
+
+    out = {
+        "metric": METRIC,
+        "value": None, "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(t_step * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "llama3_8b_down_proj_4096x14336_w4g32", "N": N, "K": K, "q": q,
+                   "group": g, "mode": args.mode, "decode_M": 1, "decode_layers": args.layers,
+                   "prefill_M": args.gemm_m, "prefill_layers": args.gemm_layers,
+                   "weights": "bf16 Student-t(5)*0.02 + 0.1% x20 outliers, seed %d" % spec.seed},
+        "wall_s": round(wall, 4),
+    }
+    if "gemv" in phases:
+        avg = t_v / n_gemv
+        gbs = gemv_bytes / avg / 1e9
+        out["value"] = round(gbs, 2)
+        out["roofline"] = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
+                           "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                           "traffic": measured_traffic("gemv"),
+                           "kernel": "gemv_kernel (ssq_matmul, M=1)",
+                           "bytes_per_launch": gemv_bytes, "avg_launch_us": round(avg * 1e6, 3)}
+    if "gemm" in phases:
+        avg = t_m / n_gemm
+        tf = gemm_flops / avg / 1e12
+        out["gemm_tflops"] = round(tf, 2)
+        out["roofline_gemm"] = {"bound": "mfma", "achieved": round(tf, 2),
+                                "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                "frac": round(tf / BF16_PEAK_TFLOPS, 4),
+                                "traffic": measured_traffic("gemm"),
+                                "kernel": f"gemm_kernel (ssq_matmul, M={args.gemm_m})",
+                                "flops_per_launch": gemm_flops, "avg_launch_us": round(avg * 1e6, 3)}
+    if "quantize" in phases:
+        avg = t_q / args.steps
+        gbs = quant_bytes / avg / 1e9
+        out["quantize_gbs"] = round(gbs, 2)
+        out["roofline_quantize"] = {"bound": "hbm", "achieved": round(gbs, 2),
+                                    "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                    "frac": round(gbs / HBM_PEAK_GBS, 4),
+                                    "traffic": measured_traffic("quantize"),
+                                    "kernel": "quantize_kernel (ssq_quantize)",
+                                    "bytes_per_launch": quant_bytes,
+                                    "avg_launch_us": round(avg * 1e6, 3)}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w_bits, x1_bits, N, K, g, q, mode, gemv_bytes / N)
+    out["host"] = platform.node()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,138 @@
+/*
+ * ssq.h -- C ABI of libssq: group-wise signed symmetric few-bit weight
+ * quantization and the weight-only dequantizing matmul, on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * Method: Colbert, Dash et al., "Signed Symmetric Quantization for Few-Bit
+ * Integers".  Argument names follow the paper's notation: q (bit width),
+ * group (g, the number of consecutive weights sharing one scale), scales (s),
+ * zp (z, the zero point).
+ *
+ * Storage format (shared by every entry point)
+ * ---------------------------------------------
+ *   W      [rows, cols]            row-major weights, groups of `group`
+ *                                  consecutive entries along cols (the
+ *                                  reduction index K of the matmul).
+ *   codes  [rows, cols*q/8] u8     row-major; field k of a row occupies bits
+ *                                  [k*q, k*q+q) of the row's little-endian bit
+ *                                  stream (q=4: byte j = u[2j] | u[2j+1]<<4).
+ *   scales [rows, cols/group] u16  IEEE binary16 bit patterns, one signed scale
+ *                                  per group (App. B.1: the Q*_0 formats store
+ *                                  s = gamma*alpha, which may be negative).
+ *   zp     [rows, cols/group] u8   integer zero point, asymmetric mode only.
+ *
+ *   Symmetric modes store the offset-binary index u = c + 2^(q-1) of the code
+ *   c in A_q = {-2^(q-1), ..., 2^(q-1)-1}; the weight is s*(u - 2^(q-1)).
+ *   The asymmetric mode stores u in {0, ..., 2^q-1}; the weight is s*(u - z).
+ *
+ * Conventions
+ *   - Every pointer is a device pointer owned by the caller.  The library
+ *     allocates nothing, frees nothing and keeps no pointer after returning.
+ *   - W, x, y and codes must be 16-byte aligned; scales 2-byte aligned.
+ *   - bf16 and fp16 tensors are passed as their uint16_t bit patterns.
+ *   - Inputs must be finite; NaN/Inf inputs give unspecified codes.
+ *   - Arguments are validated on the host before any launch.  On an error
+ *     return nothing is launched and no output byte is written.
+ *   - Calls are asynchronous; device faults surface at the caller's next
+ *     synchronisation.  Calls never abort, exit or print.
+ *   - Sizes of zero (rows or cols for quantize, M or N for matmul) are valid
+ *     and do nothing.
+ */
+#ifndef SSQ_H
+#define SSQ_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Quantization grid (Sec. 3). */
+typedef enum {
+  SSQ_SIGNED_SYM = 0,   /* signed absmax grid, sign rule of Eq. (5)            */
+  SSQ_UNSIGNED_SYM = 1, /* absmax grid with s > 0, Eq. (3)                     */
+  SSQ_ASYM = 2          /* min-max grid, Eq. (2), with a u8 zero point         */
+} ssq_mode;
+
+typedef enum {
+  SSQ_OK = 0,
+  SSQ_EINVAL = -1,      /* bad size, q, group, mode or zp/mode combination     */
+  SSQ_EALIGN = -2,      /* a pointer violates the alignment rule above         */
+  SSQ_EHIP = -3         /* the HIP runtime reported an error at launch         */
+} ssq_status;
+
+/*
+ * ssq_quantize -- quantize bf16 weights W[rows, cols] group by group.
+ *
+ * Per group of `group` consecutive weights w (Sec. 3; Eq. (1)-(5)):
+ *   SSQ_SIGNED_SYM:   M = max|w|, alpha = M / 2^(q-1), gamma = -1 if the
+ *                     largest-magnitude entry is positive and unique in
+ *                     magnitude among opposite signs (max w > -min w), else +1;
+ *                     s = gamma*alpha; c = clip(rne(fl32(w/s)), A_q).
+ *   SSQ_UNSIGNED_SYM: the same with gamma = +1 (Eq. (3)).
+ *   SSQ_ASYM:         min' = min(min w, 0), max' = max(max w, 0),
+ *                     s = fl32(fl32(max' - min') / (2^q - 1)),
+ *                     z = clip(rne(fl32(-min'/s)), 0, 2^q-1),
+ *                     u = clip(rne(fl32(w/s)) + z, 0, 2^q-1).
+ * Arithmetic is IEEE binary32 with round-half-to-even; the stored scale is
+ * binary16(s) rounded half to even.  A group whose scale would be zero (all
+ * entries zero) stores scale +0 and code 0 (index 2^(q-1), or 0 for ASYM).
+ *
+ *   W      device, bf16 bits [rows, cols] row-major, read only
+ *   rows   >= 0, number of weight rows (output channels N)
+ *   cols   >= 0, multiple of group (reduction length K)
+ *   group  32, 64 or 128
+ *   q      2, 3 or 4
+ *   mode   ssq_mode
+ *   codes  device, u8 [rows, cols*q/8], written
+ *   scales device, u16 [rows, cols/group], written
+ *   zp     device, u8 [rows, cols/group], written; must be non-NULL iff
+ *          mode == SSQ_ASYM
+ * Enqueued on the null stream.  Returns SSQ_OK or a negative ssq_status.
+ */
+int ssq_quantize(const uint16_t* W, int64_t rows, int64_t cols, int group, int q, int mode,
+                 uint8_t* codes, uint16_t* scales, uint8_t* zp);
+
+/* ssq_quantize for binary32 weights W[rows, cols]; otherwise identical. */
+int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int q, int mode,
+                     uint8_t* codes, uint16_t* scales, uint8_t* zp);
+
+/*
+ * ssq_matmul -- y[M, N] = x[M, K] * What[N, K]^T, where What is the
+ * dequantized weight (App. B.3):
+ *   What[n, k] = fp32(scales[n, b]) * (u[n, k] - o[n, b]),   b = k / group,
+ *   o = 2^(q-1) when zp == NULL (symmetric formats, signed or not: the sign
+ *   lives in the scale, so both run the same kernel), o = zp[n, b] otherwise.
+ * Products accumulate in fp32; y is rounded to bf16 (half to even).
+ * M = 1 runs a streaming GEMV; larger M runs a tiled kernel that dequantizes
+ * weight tiles into LDS and multiplies them with bf16 MFMA.
+ *
+ *   x      device, bf16 bits [M, K] row-major, read only
+ *   M      >= 0, number of activation rows (tokens)
+ *   codes  device, u8 [N, K*q/8] as written by ssq_quantize
+ *   scales device, u16 [N, K/group]
+ *   zp     device, u8 [N, K/group] for the asymmetric format, else NULL
+ *   N      >= 0, number of weight rows (outputs)
+ *   K      > 0, multiple of group
+ *   group  32, 64 or 128;  q  2, 3 or 4
+ *   y      device, bf16 bits [M, N] row-major, written
+ *   stream HIP stream the kernels are enqueued on (NULL: null stream)
+ */
+int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+               const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+               hipStream_t stream);
+
+/* ssq_matmul with binary32 x[M, K] and y[M, N] (fp32 accumulation and output). */
+int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                   const uint8_t* zp, int64_t N, int64_t K, int group, int q, float* y,
+                   hipStream_t stream);
+
+/* Static description of a status code; never NULL. */
+const char* ssq_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSQ_H */

@@ -1,0 +1,90 @@
+// C ABI of libssq: argument validation and kernel dispatch (see include/ssq.h).
+//
+// Every check runs on the host before any HIP call, so an invalid call returns
+// without launching anything or touching an output byte.
+#include "ssq.h"
+
+#include "ssq_internal.h"
+
+namespace {
+
+constexpr int64_t kMaxElems = int64_t(1) << 40;   // rows*cols or N*K
+constexpr int64_t kMaxDim = int64_t(1) << 30;     // any single dimension (kernels index in int)
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+bool valid_q(int q) { return q == 2 || q == 3 || q == 4; }
+bool valid_group(int g) { return g == 32 || g == 64 || g == 128; }
+int status_of(hipError_t e) { return e == hipSuccess ? SSQ_OK : SSQ_EHIP; }
+
+int check_quantize(const void* W, int64_t rows, int64_t cols, int group, int q, int mode,
+                   const uint8_t* codes, const uint16_t* scales, const uint8_t* zp) {
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return SSQ_EINVAL;
+  if (!valid_q(q) || !valid_group(group)) return SSQ_EINVAL;
+  if (mode != SSQ_SIGNED_SYM && mode != SSQ_UNSIGNED_SYM && mode != SSQ_ASYM) return SSQ_EINVAL;
+  if (cols % group != 0) return SSQ_EINVAL;
+  if ((mode == SSQ_ASYM) != (zp != nullptr)) return SSQ_EINVAL;
+  if (rows * cols > kMaxElems) return SSQ_EINVAL;
+  if (rows == 0 || cols == 0) return SSQ_OK;
+  if (W == nullptr || codes == nullptr || scales == nullptr) return SSQ_EINVAL;
+  if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 2)) return SSQ_EALIGN;
+  return SSQ_OK;
+}
+
+int check_matmul(const void* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                 int64_t N, int64_t K, int group, int q, const void* y) {
+  if (M < 0 || N < 0 || K <= 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return SSQ_EINVAL;
+  if (!valid_q(q) || !valid_group(group) || K % group != 0) return SSQ_EINVAL;
+  if (N * K > kMaxElems || M * K > kMaxElems || M * N > kMaxElems) return SSQ_EINVAL;
+  if (M == 0 || N == 0) return SSQ_OK;
+  if (x == nullptr || codes == nullptr || scales == nullptr || y == nullptr) return SSQ_EINVAL;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(y, 16) || !aligned(scales, 2))
+    return SSQ_EALIGN;
+  return SSQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ssq_quantize(const uint16_t* W, int64_t rows, int64_t cols, int group, int q, int mode,
+                 uint8_t* codes, uint16_t* scales, uint8_t* zp) {
+  const int st = check_quantize(W, rows, cols, group, q, mode, codes, scales, zp);
+  if (st != SSQ_OK || rows == 0 || cols == 0) return st;
+  return status_of(ssq::launch_quantize_bf16(W, rows, cols, group, q, mode, codes, scales, zp, nullptr));
+}
+
+int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int q, int mode,
+                     uint8_t* codes, uint16_t* scales, uint8_t* zp) {
+  const int st = check_quantize(W, rows, cols, group, q, mode, codes, scales, zp);
+  if (st != SSQ_OK || rows == 0 || cols == 0) return st;
+  return status_of(ssq::launch_quantize_f32(W, rows, cols, group, q, mode, codes, scales, zp, nullptr));
+}
+
+int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+               const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+               hipStream_t stream) {
+  const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
+  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, stream));
+}
+
+int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                   const uint8_t* zp, int64_t N, int64_t K, int group, int q, float* y,
+                   hipStream_t stream) {
+  const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  return status_of(ssq::launch_matmul_f32(x, M, codes, scales, zp, N, K, group, q, y, stream));
+}
+
+const char* ssq_strerror(int status) {
+  switch (status) {
+    case SSQ_OK: return "success";
+    case SSQ_EINVAL: return "invalid argument (size, q, group, mode or zero-point/mode mismatch)";
+    case SSQ_EALIGN: return "misaligned pointer (W, x, y, codes need 16 bytes; scales 2)";
+    case SSQ_EHIP: return "HIP runtime error at kernel launch";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,130 @@
+"""Thin Python binding of libssq's C ABI (argument marshalling only).
+
+Every step of the quantize / matmul path runs in the HIP kernels behind
+``libssq.so``; this module only checks tensor dtypes and shapes, allocates
+output tensors with torch and passes device pointers and the current stream.
+It fails loudly if the library has not been built: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+SIGNED_SYM, UNSIGNED_SYM, ASYM = 0, 1, 2
+MODES = {"signed_sym": SIGNED_SYM, "unsigned_sym": UNSIGNED_SYM, "asym": ASYM}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libssq.so")
+
+_EXPORTS = {
+    "ssq_quantize": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                    ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_void_p]),
+    "ssq_quantize_f32": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p]),
+    "ssq_matmul": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                  ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]),
+    "ssq_matmul_f32": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                      ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                      ctypes.c_void_p]),
+    "ssq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class SSQError(RuntimeError):
+    """A libssq call returned a non-zero ssq_status."""
+
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {ssq_strerror(status)} (status {status})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load libssq.so (once) and declare its signatures; raises if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2607_08779_amd.build` (no fallback exists)")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _EXPORTS.items():
+            fn = getattr(handle, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = handle
+    return _lib
+
+
+def ssq_strerror(status: int) -> str:
+    return lib().ssq_strerror(int(status)).decode()
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise SSQError(fn, status)
+
+
+def ssq_quantize(W: torch.Tensor, group: int, q: int, mode: int,
+                 out: Optional[Tuple[torch.Tensor, torch.Tensor, Optional[torch.Tensor]]] = None):
+    """Quantize W [rows, cols] (bf16 or fp32, on the GPU) group-wise.
+
+    Returns (codes u8 [rows, cols*q/8], scales int16 [rows, cols/group] holding
+    binary16 bit patterns, zp u8 [rows, cols/group] for ASYM else None).
+    Runs on the null stream, like the C entry point.
+    """
+    if W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be a contiguous 2-D tensor")
+    if W.dtype == torch.bfloat16:
+        fn = "ssq_quantize"
+    elif W.dtype == torch.float32:
+        fn = "ssq_quantize_f32"
+    else:
+        raise TypeError("W must be bfloat16 or float32")
+    rows, cols = W.shape
+    if out is None:
+        codes = torch.empty((rows, cols * q // 8), dtype=torch.uint8, device=W.device)
+        scales = torch.empty((rows, cols // group if group else 0), dtype=torch.int16, device=W.device)
+        zp = (torch.empty((rows, cols // group if group else 0), dtype=torch.uint8, device=W.device)
+              if mode == ASYM else None)
+    else:
+        codes, scales, zp = out
+    st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, mode, _ptr(codes), _ptr(scales), _ptr(zp))
+    _check(fn, st)
+    return codes, scales, zp
+
+
+def ssq_matmul(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
+               zp: Optional[torch.Tensor], N: int, K: int, group: int, q: int,
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y [M, N] = x [M, K] @ dequant(codes, scales, zp)^T on the current stream.
+
+    x bf16 gives y bf16 (``ssq_matmul``); x fp32 gives y fp32 (``ssq_matmul_f32``).
+    """
+    if x.dim() != 2 or not x.is_contiguous() or x.shape[1] != K:
+        raise ValueError("x must be a contiguous [M, K] tensor")
+    if x.dtype == torch.bfloat16:
+        fn = "ssq_matmul"
+    elif x.dtype == torch.float32:
+        fn = "ssq_matmul_f32"
+    else:
+        raise TypeError("x must be bfloat16 or float32")
+    M = x.shape[0]
+    y = torch.empty((M, N), dtype=x.dtype, device=x.device) if out is None else out
+    st = getattr(lib(), fn)(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
+                            _ptr(y), _stream(x.device))
+    _check(fn, st)
+    return y

@@ -1,0 +1,97 @@
+"""Host-only checks of the C ABI: the library loads, exports every declared symbol
+and rejects invalid arguments before any HIP call (no kernel is launched here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_08779_amd import ssq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ssq.h")
+
+EINVAL, EALIGN = -1, -2
+P16 = ctypes.c_void_p(1 << 20)      # aligned dummy pointers: never dereferenced, because
+P2 = ctypes.c_void_p((1 << 20) + 2)  # every call below fails validation first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ssq_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_quantize",
+                                    "ssq_quantize_f32", "ssq_strerror"]
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ssq.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_strerror_never_null():
+    for st in (0, -1, -2, -3, 7, -99):
+        assert isinstance(ssq.ssq_strerror(st), str) and ssq.ssq_strerror(st)
+
+
+@pytest.mark.parametrize("args", [
+    dict(q=5), dict(q=1), dict(group=16), dict(group=48), dict(mode=3), dict(mode=-1),
+    dict(cols=48), dict(rows=-1), dict(cols=-32), dict(mode=2),          # ASYM without zp
+    dict(zp=P16),                                                         # zp with a sym mode
+    dict(W=None), dict(codes=None), dict(scales=None),
+])
+def test_quantize_rejects_invalid_arguments(args):
+    a = dict(W=P16, rows=4, cols=64, group=32, q=4, mode=0, codes=P16, scales=P16, zp=None)
+    a.update(args)
+    for fn in (ssq.lib().ssq_quantize, ssq.lib().ssq_quantize_f32):
+        assert fn(a["W"], a["rows"], a["cols"], a["group"], a["q"], a["mode"], a["codes"],
+                  a["scales"], a["zp"]) == EINVAL
+
+
+@pytest.mark.parametrize("which", ["W", "codes", "scales"])
+def test_quantize_rejects_misaligned_pointers(which):
+    a = dict(W=P16, codes=P16, scales=P16)
+    a[which] = ctypes.c_void_p((1 << 20) + (1 if which == "scales" else 8))
+    st = ssq.lib().ssq_quantize(a["W"], 4, 64, 32, 4, 0, a["codes"], a["scales"], None)
+    assert st == EALIGN
+
+
+def test_quantize_empty_is_a_noop():
+    for rows, cols in ((0, 64), (4, 0), (0, 0)):
+        assert ssq.lib().ssq_quantize(None, rows, cols, 32, 4, 0, None, None, None) == 0
+
+
+@pytest.mark.parametrize("args", [
+    dict(K=0), dict(K=48), dict(K=-32), dict(M=-1), dict(N=-1), dict(q=8), dict(group=96),
+    dict(x=None), dict(codes=None), dict(scales=None), dict(y=None),
+])
+def test_matmul_rejects_invalid_arguments(args):
+    a = dict(x=P16, M=2, codes=P16, scales=P16, zp=None, N=8, K=64, group=32, q=4, y=P16)
+    a.update(args)
+    for fn in (ssq.lib().ssq_matmul, ssq.lib().ssq_matmul_f32):
+        assert fn(a["x"], a["M"], a["codes"], a["scales"], a["zp"], a["N"], a["K"], a["group"],
+                  a["q"], a["y"], None) == EINVAL
+
+
+@pytest.mark.parametrize("which", ["x", "codes", "y", "scales"])
+def test_matmul_rejects_misaligned_pointers(which):
+    a = dict(x=P16, codes=P16, y=P16, scales=P16)
+    a[which] = P2 if which != "scales" else ctypes.c_void_p((1 << 20) + 1)
+    st = ssq.lib().ssq_matmul(a["x"], 2, a["codes"], a["scales"], None, 8, 64, 32, 4, a["y"], None)
+    assert st == EALIGN
+
+
+def test_matmul_empty_is_a_noop():
+    for M, N in ((0, 8), (2, 0)):
+        assert ssq.lib().ssq_matmul(None, M, None, None, None, N, 64, 32, 4, None, None) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(ssq, "LIB_PATH", "/nonexistent/libssq.so")
+    monkeypatch.setattr(ssq, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        ssq.lib()

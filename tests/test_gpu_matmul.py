@@ -1,0 +1,184 @@
+"""GPU parity: ssq_matmul (GEMV at M = 1, MFMA GEMM at M >= 2) and ssq_matmul_f32
+against the binary64 CPU oracle.
+
+Tolerances (relative L2 over the compared outputs): 2e-2 for bf16 output and
+1e-3 for the binary32 path.  The GEMV, which keeps the weights exact and only
+rounds its fp32 result to bf16, is also held to an elementwise bound of one
+bf16 rounding plus fp32 accumulation slack.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ssq_oracle as O
+from paper_2607_08779_amd import ssq, synth
+from tests.parity_common import (assert_quant_equal, log_metric, rel_l2, sample_rows, to_device,
+                                 weights_host, widen, y_to_f64)
+
+pytestmark = pytest.mark.gpu
+
+MODES = [O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM]
+TOL_BF16 = 2e-2
+TOL_F32 = 1e-3
+
+
+def check_matmul(w_host, x_host, group, q, mode, rows_idx=None, bf16_w=True, bf16_x=True, tag=""):
+    """Quantize on the GPU, multiply on the GPU, compare with the oracle on rows_idx."""
+    N, K = w_host.shape
+    W = to_device(w_host, bf16_w)
+    codes, scales, zp = ssq.ssq_quantize(W, group, q, mode)
+    X = to_device(x_host, bf16_x)
+    y = ssq.ssq_matmul(X, codes, scales, zp, N, K, group, q)
+    torch.cuda.synchronize()
+    sel = np.arange(N) if rows_idx is None else rows_idx
+    ref_q = O.quantize(widen(w_host[sel], bf16_w), group, q, mode)
+    assert_quant_equal((codes, scales, zp), ref_q, None if rows_idx is None else sel, tag=tag)
+    xr = widen(x_host, bf16_x)
+    y_ref = O.matmul(xr, ref_q.codes, ref_q.scales, ref_q.zp, len(sel), K, group, q)
+    y_gpu = y_to_f64(y)[:, sel]
+    err = rel_l2(y_gpu, y_ref)
+    M = x_host.shape[0]
+    log_metric(test=tag, M=M, N=N, K=K, q=q, group=group, mode=mode, rel_l2=err,
+               dtype="bf16" if bf16_x else "f32")
+    tol = TOL_BF16 if bf16_x else TOL_F32
+    assert err <= tol, f"{tag}: rel L2 {err:.3e} > {tol}"
+    if bf16_x and M == 1:
+        slack = 2.0 ** -8 * np.abs(y_ref) + 1e-4 * np.sqrt(np.mean(y_ref ** 2))
+        bad = np.abs(y_gpu - y_ref) > slack
+        assert not bad.any(), f"{tag}: {bad.sum()} outputs beyond one bf16 rounding"
+    return err
+
+
+def rand_w(N, K, seed, bf16=True):
+    return synth.weights(synth.WeightSpec(N, K, nu=5.0, scale=0.02, outlier_frac=0.001,
+                                          seed=seed, bf16=bf16))
+
+
+# ---------------------------------------------------------------------------
+# Small and ragged cases, every format.
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("mode", MODES)
+def test_gemv_small_all_formats(q, group, mode):
+    w = rand_w(37, 1536, seed=10 * q + group)
+    x = synth.activations(1, 1536, seed=q)
+    check_matmul(w, x, group, q, mode, tag="gemv 37x1536")
+
+
+@pytest.mark.parametrize("K", [32, 64, 4096 + 32])
+def test_gemv_odd_reduction_lengths(K):
+    w = rand_w(9, K, seed=K)
+    x = synth.activations(1, K, seed=K)
+    for mode in MODES:
+        check_matmul(w, x, 32, 4, mode, tag=f"gemv K={K}")
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 128])
+@pytest.mark.parametrize("mode", MODES)
+def test_gemm_ragged_all_formats(q, group, mode):
+    # M=200, N=300 leave partial 128x128 tiles in both directions; at g=32, K=1056 is an odd
+    # number of 32-blocks (half of the last 64-deep step is empty)
+    K = 1056 if group == 32 else 1152
+    w = rand_w(300, K, seed=7 * q + group)
+    x = synth.activations(200, K, seed=q + group)
+    check_matmul(w, x, group, q, mode, tag=f"gemm 200x300x{K}")
+
+
+@pytest.mark.parametrize("M", [2, 3, 16, 129])
+def test_gemm_small_token_counts(M):
+    w = rand_w(64, 512, seed=M)
+    x = synth.activations(M, 512, seed=M)
+    check_matmul(w, x, 32, 4, O.SIGNED_SYM, tag=f"gemm M={M}")
+
+
+@pytest.mark.parametrize("M", [1, 3, 5])
+@pytest.mark.parametrize("mode", MODES)
+def test_f32_path(M, mode):
+    spec = synth.small_fp32().layers["w"]
+    w = weights_host(spec)
+    x = synth.activations(M, 512, seed=1100 + M, bf16=False)
+    check_matmul(w, x, 32, 4, mode, bf16_w=False, bf16_x=False, tag=f"f32 256x512 M={M}")
+
+
+def test_f32_path_other_formats():
+    w = synth.weights(synth.WeightSpec(50, 768, nu=4.0, scale=0.02, seed=8, bf16=False))
+    x = synth.activations(2, 768, seed=8, bf16=False)
+    for q in (2, 3):
+        for group in (64, 128):
+            check_matmul(w, x, group, q, O.ASYM, bf16_w=False, bf16_x=False, tag="f32 other")
+
+
+def test_zero_weights_give_zero_output():
+    w = np.zeros((16, 256), np.uint16)
+    for M in (1, 4):
+        x = synth.activations(M, 256, seed=M)
+        for mode in MODES:
+            W = to_device(w, True)
+            codes, scales, zp = ssq.ssq_quantize(W, 32, 4, mode)
+            y = ssq.ssq_matmul(to_device(x, True), codes, scales, zp, 16, 256, 32, 4)
+            torch.cuda.synchronize()
+            assert (y.float() == 0).all()
+
+
+def test_empty_matmul_is_a_noop():
+    codes = torch.zeros((8, 32), dtype=torch.uint8, device="cuda")
+    scales = torch.zeros((8, 2), dtype=torch.int16, device="cuda")
+    y = ssq.ssq_matmul(torch.zeros((0, 64), dtype=torch.bfloat16, device="cuda"),
+                       codes, scales, None, 8, 64, 32, 4)
+    assert y.shape == (0, 8)
+    y = ssq.ssq_matmul(torch.zeros((3, 64), dtype=torch.bfloat16, device="cuda"),
+                       codes, scales, None, 0, 64, 32, 4)
+    torch.cuda.synchronize()
+    assert y.shape == (3, 0)
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads (sampled output columns).
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("mode", MODES)
+def test_llama3_8b_decode_gemv_full_size(mode):
+    wl = synth.llama3_8b_decode()
+    for name, spec in wl.layers.items():
+        w = weights_host(spec)
+        x = synth.activations(1, spec.cols, seed=wl.x_seed)
+        check_matmul(w, x, 32, 4, mode, rows_idx=sample_rows(spec.rows, seed=spec.seed),
+                     tag=f"decode {name}")
+
+
+@pytest.mark.parametrize("q", [2, 3])
+@pytest.mark.parametrize("group", [32, 128])
+def test_llama3_8b_block_gemv_full_size(q, group):
+    wl = synth.llama3_8b_block()
+    for name in ("k_proj", "gate_proj", "down_proj"):
+        spec = wl.layers[name]
+        w = weights_host(spec)
+        x = synth.activations(1, spec.cols, seed=wl.x_seed)
+        for mode in MODES:
+            check_matmul(w, x, group, q, mode, rows_idx=sample_rows(spec.rows, n=24, seed=1),
+                         tag=f"block {name}")
+
+
+@pytest.mark.parametrize("M", [512, 2048])
+@pytest.mark.parametrize("layer", ["gate_proj", "down_proj"])
+def test_prefill_gemm_full_size(M, layer):
+    wl = synth.prefill()
+    spec = wl.layers[layer]
+    w = weights_host(spec)
+    x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
+    check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=32, seed=M),
+                 tag=f"prefill {layer} M={M}")
+
+
+@pytest.mark.parametrize("M", [1, 16])
+def test_llama3_70b_matmul_full_size(M):
+    wl = synth.llama3_70b_block()
+    for name in ("k_proj", "down_proj"):
+        spec = wl.layers[name]
+        w = synth.weights(spec)
+        x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
+        check_matmul(w, x, 32, 2, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=24, seed=M),
+                     tag=f"70b {name} M={M}")
