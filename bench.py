@@ -224,7 +224,7 @@ def main() -> int:
         "config": {"workload": "llama3_8b_down_proj_4096x14336_w4g32", "N": N, "K": K, "q": q,
                    "group": g, "mode": args.mode, "decode_M": 1, "decode_layers": args.layers,
                    "prefill_M": args.gemm_m, "prefill_layers": args.gemm_layers,
-                   "weights": "bf16 Student-t(5)*0.02 + 0.1% x20 outliers, seed %d" % spec.seed},
+                   "weights": f"bf16 Student-t(5)*0.02 + 0.1% x20 outliers, seed {spec.seed}"},
         "wall_s": round(wall, 4),
     }
     if "gemv" in phases:

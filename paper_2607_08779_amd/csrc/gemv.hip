@@ -13,6 +13,8 @@
 // (0x4300 | u == 128 + u exactly), and v_dot2_f32_bf16 multiplies them with
 // activation pairs in fp32.  The 128 + o offset is removed once per block with
 // the block's activation sum, and the scale is applied once per block.
+#include <algorithm>
+
 #include "ssq_internal.h"
 
 namespace ssq {
@@ -63,88 +65,100 @@ __device__ __forceinline__ void permute_x(const uint32_t (&X)[16], uint32_t (&xp
   }
 }
 
-// sum_{k in block} x[k] * (128 + u[k]) in fp32.
+// sum_{k in block} x[k] * (128 + u[k]) in fp32.  `magic` holds kMagic (in a VGPR).
 template <int Q>
-__device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&xp)[16]) {
+__device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&xp)[16], uint32_t magic) {
   float acc = 0.0f;
   if constexpr (Q == 4) {
 #pragma unroll
-    for (int d = 0; d < 4; ++d)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc = dot2(((b.d[d] >> (4 * j)) & 0x000F000Fu) | kMagic, xp[4 * d + j], acc);
+    for (int d = 0; d < 4; ++d) {
+      const uint32_t w4 = b.d[d] >> 4;
+      acc = dot2(and_or(b.d[d], 0x000F000Fu, magic), xp[4 * d], acc);
+      acc = dot2(and_or(w4, 0x000F000Fu, magic), xp[4 * d + 1], acc);
+      acc = dot2(and_or(b.d[d] >> 8, 0x000F000Fu, magic), xp[4 * d + 2], acc);
+      acc = dot2(and_or(w4 >> 8, 0x000F000Fu, magic), xp[4 * d + 3], acc);
+    }
   } else if constexpr (Q == 2) {
 #pragma unroll
     for (int d = 0; d < 2; ++d)
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        acc = dot2(((b.d[d] >> (2 * j)) & 0x00030003u) | kMagic, xp[8 * d + j], acc);
+        acc = dot2(and_or(b.d[d] >> (2 * j), 0x00030003u, magic), xp[8 * d + j], acc);
   } else {
     // Re-split the 96 bits into four 24-bit words of 8 fields, then move fields 4..7 of
     // each word up to bit 16 so that pairs (e_j, e_{j+4}) share one shift.
-    const uint32_t v[4] = {b.d[0] & 0xFFFFFFu, __builtin_amdgcn_alignbit(b.d[1], b.d[0], 24) & 0xFFFFFFu,
-                           __builtin_amdgcn_alignbit(b.d[2], b.d[1], 16) & 0xFFFFFFu, b.d[2] >> 8};
+    const uint32_t v[4] = {b.d[0], __builtin_amdgcn_alignbit(b.d[1], b.d[0], 24),
+                           __builtin_amdgcn_alignbit(b.d[2], b.d[1], 16), b.d[2] >> 8};
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const uint32_t s = (v[w] & 0xFFFu) | ((v[w] << 4) & 0x0FFF0000u);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc = dot2(((s >> (3 * j)) & 0x00070007u) | kMagic, xp[4 * w + j], acc);
+      for (int j = 0; j < 4; ++j) acc = dot2(and_or(s >> (3 * j), 0x00070007u, magic), xp[4 * w + j], acc);
     }
   }
   return acc;
 }
 
-template <int Q, int G, bool ZP, int R, int U>
-__global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ x,
-                                                   const uint8_t* __restrict__ codes,
-                                                   const uint16_t* __restrict__ scales,
-                                                   const uint8_t* __restrict__ zp, int N, int K,
-                                                   uint16_t* __restrict__ y) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * R;
-  if (row0 >= N) return;  // whole wavefront
-  const int nblk = K / 32;
-  const int64_t row_bytes = (int64_t)K * Q / 8;
-  const int groups_per_row = K / G;
+// Work split.  A team of T threads (T = blocks per row rounded up to whole
+// wavefronts, at most 1024) owns kRows consecutive rows; thread t takes block t of
+// each row (and t + T, ... for rows longer than 1024 blocks).  Short rows pack
+// several teams into one 256-thread workgroup.  Each thread issues its activation
+// load and its kRows code and scale loads before any arithmetic and consumes them
+// in issue order, so many small wavefronts stream and compute concurrently.
+// Partial sums meet through a DPP wavefront reduction and LDS.
+constexpr int kRows = 4;
+constexpr int kMaxWaves = 16;
+
+template <int Q, int G, bool ZP>
+__global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__ x,
+                                                    const uint8_t* __restrict__ codes,
+                                                    const uint16_t* __restrict__ scales,
+                                                    const uint8_t* __restrict__ zp, int N, int K,
+                                                    int team_threads, uint16_t* __restrict__ y) {
   constexpr int kBlocksPerGroup = G / 32;
   constexpr float kSymOffset = kMagicValue + (float)(1 << (Q - 1));
+  __shared__ float partial[kMaxWaves][kRows];
 
-  float yacc[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) yacc[r] = 0.0f;
+  // team_threads is a multiple of 64, so the team index is uniform across a wavefront.
+  const int team = __builtin_amdgcn_readfirstlane((int)threadIdx.x / team_threads);
+  const int t = (int)threadIdx.x - team * team_threads;
+  const int teams = blockDim.x / team_threads;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row0 = ((int64_t)blockIdx.x * teams + team) * kRows;
+  const int nblk = K / 32;
+  const uint32_t row_bytes = (uint32_t)K * Q / 8;
+  const uint32_t groups_per_row = (uint32_t)(K / G);
+  const uint32_t magic = kMagic;
 
-  for (int j0 = lane; j0 < nblk; j0 += 64 * U) {
-    Block<Q> cb[U][R];
-    float sc[U][R], off[U][R];
+  float yacc[kRows];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = j0 + 64 * u;
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        const int64_t row = row0 + r;
-        if (j < nblk && row < N) {
-          cb[u][r] = load_block<Q>(codes + row * row_bytes + (int64_t)j * (4 * Q));
-          const int64_t gi = row * groups_per_row + j / kBlocksPerGroup;
-          sc[u][r] = f16_bits_to_f32(scales[gi]);
-          off[u][r] = ZP ? kMagicValue + (float)zp[gi] : kSymOffset;
-        } else {
-#pragma unroll
-          for (int i = 0; i < Q; ++i) cb[u][r].d[i] = 0;
-          sc[u][r] = 0.0f;
-          off[u][r] = 0.0f;
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = j0 + 64 * u;
-      if (j >= nblk) break;
+  for (int r = 0; r < kRows; ++r) yacc[r] = 0.0f;
+
+  if (row0 < N) {
+    // Descriptors cover exactly this team's rows: loads of rows past N return zeros
+    // (zero codes and zero scales contribute nothing).
+    const uint32_t rows_here = (uint32_t)(N - row0 < kRows ? N - row0 : kRows);
+    const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + row0 * row_bytes, rows_here * row_bytes);
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + row0 * groups_per_row, rows_here * groups_per_row * 2);
+    const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + row0 * groups_per_row : zp, ZP ? rows_here * groups_per_row : 0);
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
+    for (int j = t; j < nblk; j += team_threads) {
+      // Loads first, in consumption order: the activation block, then per row its codes,
+      // scale (and zero point).  Row offsets are scalar, lane offsets shared by all rows.
       uint32_t X[16];
-      const uint4* xv = reinterpret_cast<const uint4*>(x) + (int64_t)j * 4;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const uint4 t = xv[i];
-        X[4 * i] = t.x; X[4 * i + 1] = t.y; X[4 * i + 2] = t.z; X[4 * i + 3] = t.w;
+        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rx, j * 64 + 16 * i, 0, 0);
+        X[4 * i] = v.x; X[4 * i + 1] = v.y; X[4 * i + 2] = v.z; X[4 * i + 3] = v.w;
+      }
+      Block<Q> cb[kRows];
+      uint32_t sbits[kRows], zbits[kRows];
+      const uint32_t goff = (uint32_t)(j / kBlocksPerGroup);
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        buffer_block_codes<Q>(rc, (uint32_t)j * (4 * Q), r * row_bytes, cb[r].d);
+        sbits[r] = __builtin_amdgcn_raw_buffer_load_b16(rs, goff * 2, r * groups_per_row * 2, 0);
+        zbits[r] = ZP ? __builtin_amdgcn_raw_buffer_load_b8(rz, goff, r * groups_per_row, 0) : 0u;
       }
       float xs = 0.0f;  // sum of the block's activations
 #pragma unroll
@@ -152,16 +166,28 @@ __global__ __launch_bounds__(256) void gemv_kernel(const uint16_t* __restrict__ 
       uint32_t xp[16];
       permute_x<Q>(X, xp);
 #pragma unroll
-      for (int r = 0; r < R; ++r) {
-        const float acc = block_dot<Q>(cb[u][r], xp);
-        yacc[r] = __builtin_fmaf(sc[u][r], __builtin_fmaf(-off[u][r], xs, acc), yacc[r]);
+      for (int r = 0; r < kRows; ++r) {
+        const float acc = block_dot<Q>(cb[r], xp, magic);
+        const float sc = f16_bits_to_f32(sbits[r]);
+        const float off = ZP ? kMagicValue + (float)zbits[r] : kSymOffset;
+        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
       }
     }
   }
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const float v = group_sum<64>(yacc[r]);
-    if (lane == 0 && row0 + r < N) y[row0 + r] = f32_to_bf16_bits(v);
+  for (int r = 0; r < kRows; ++r) {
+    const float v = wave_sum(yacc[r]);
+    if (lane == 63) partial[wave][r] = v;
+  }
+  __syncthreads();
+  if (t < kRows) {
+    const int64_t row = row0 + t;
+    if (row < N) {
+      const int waves_per_team = team_threads / 64;
+      float v = 0.0f;
+      for (int w = 0; w < waves_per_team; ++w) v += partial[team * waves_per_team + w][t];
+      y[row] = f32_to_bf16_bits(v);
+    }
   }
 }
 
@@ -213,9 +239,13 @@ __global__ __launch_bounds__(256) void matmul_f32_kernel(const float* __restrict
 template <int Q, int G, bool ZP>
 hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
                          const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
-  constexpr int R = 2, U = 2;
-  const dim3 grid((unsigned)((N + 4 * R - 1) / (4 * R)));
-  gemv_kernel<Q, G, ZP, R, U><<<grid, 256, 0, stream>>>(x, codes, scales, zp, (int)N, (int)K, y);
+  const int64_t nblk = K / 32;
+  const int team = (int)std::min<int64_t>(1024, (nblk + 63) / 64 * 64);
+  const int teams = team >= 256 ? 1 : 256 / team;
+  const int64_t rows_per_block = (int64_t)teams * kRows;
+  const dim3 grid((unsigned)((N + rows_per_block - 1) / rows_per_block));
+  gemv_kernel<Q, G, ZP><<<grid, team * teams, 0, stream>>>(x, codes, scales, zp, (int)N, (int)K,
+                                                           team, y);
   return hipGetLastError();
 }
 

@@ -24,6 +24,41 @@ __device__ __forceinline__ uint32_t load_stream4(const void* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p));
 }
 
+// Raw buffer descriptors: base address + byte count (gfx9 word 3).  A load at or past
+// the byte count returns zeros, which serves as free predication at ragged edges.
+typedef uint32_t u32x3 __attribute__((ext_vector_type(3)));
+constexpr int kBufferWord3 = 0x00020000;
+constexpr int kStream = 2;   // cache policy bits: non-temporal (data read once)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferWord3);
+}
+
+// Codes of one 32-weight block (4q bytes) from a buffer, as q dwords.
+template <int Q>
+__device__ __forceinline__ void buffer_block_codes(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                                   uint32_t (&d)[Q]) {
+  if constexpr (Q == 4) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, kStream);
+    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+  } else if constexpr (Q == 2) {
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, (int)soff, kStream);
+    d[0] = v.x; d[1] = v.y;
+  } else {
+    const u32x3 v = __builtin_amdgcn_raw_buffer_load_b96(r, (int)voff, (int)soff, kStream);
+    d[0] = v.x; d[1] = v.y; d[2] = v.z;
+  }
+}
+
+// (v & mask) | magic in one v_and_or_b32.  gfx9 VOP3 encodings take no literals and
+// read one SGPR, so the mask rides in an SGPR and the magic in a VGPR; left to itself
+// the compiler emits separate and/or instructions.
+__device__ __forceinline__ uint32_t and_or(uint32_t v, uint32_t mask, uint32_t magic) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "s"(mask), "v"(magic));
+  return r;
+}
+
 // Codes of one 32-weight block (4q bytes) as q dwords.
 template <int Q>
 __device__ __forceinline__ void load_block_codes(const uint8_t* p, uint32_t (&d)[Q]) {
@@ -71,6 +106,24 @@ template <int WIDTH>
 __device__ __forceinline__ float group_max(float v) {
 #pragma unroll
   for (int o = 1; o < WIDTH; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Sum over a whole wavefront; the total lands in lane 63.  Row-local DPP steps
+// (quad_perm, half-mirror, mirror), then row_bcast:15 / row_bcast:31 carry the row
+// sums across the four 16-lane rows.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add(float v) {
+  const int moved = __builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false);
+  return v + __int_as_float(moved);
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1,0,3,2]
+  v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2,3,0,1]
+  v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
+  v = dpp_add<0x140, 0xF>(v);   // row_mirror
+  v = dpp_add<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+  v = dpp_add<0x143, 0xC>(v);   // row_bcast:31 into rows 2 and 3
   return v;
 }
 
