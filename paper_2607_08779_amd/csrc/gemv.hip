@@ -106,7 +106,13 @@ __device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&x
 // load and its kRows code and scale loads before any arithmetic and consumes them
 // in issue order, so many small wavefronts stream and compute concurrently.
 // Partial sums meet through a DPP wavefront reduction and LDS.
-constexpr int kRows = 4;
+#ifndef SSQ_GEMV_ROWS
+#define SSQ_GEMV_ROWS 4          // rows per team
+#endif
+#ifndef SSQ_GEMV_BLOCKS_PER_THREAD
+#define SSQ_GEMV_BLOCKS_PER_THREAD 1
+#endif
+constexpr int kRows = SSQ_GEMV_ROWS;
 constexpr int kMaxWaves = 16;
 
 template <int Q, int G, bool ZP>
@@ -240,7 +246,8 @@ template <int Q, int G, bool ZP>
 hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
                          const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
   const int64_t nblk = K / 32;
-  const int team = (int)std::min<int64_t>(1024, (nblk + 63) / 64 * 64);
+  const int64_t per_thread = SSQ_GEMV_BLOCKS_PER_THREAD;
+  const int team = (int)std::min<int64_t>(1024, ((nblk + per_thread - 1) / per_thread + 63) / 64 * 64);
   const int teams = team >= 256 ? 1 : 256 / team;
   const int64_t rows_per_block = (int64_t)teams * kRows;
   const dim3 grid((unsigned)((N + rows_per_block - 1) / rows_per_block));

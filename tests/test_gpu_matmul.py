@@ -135,6 +135,31 @@ def test_empty_matmul_is_a_noop():
     assert y.shape == (3, 0)
 
 
+@pytest.mark.parametrize("M", [1, 64])
+def test_graph_replay_matches_eager(M):
+    """ssq_matmul captured in a HIP graph: every replay, with eager work in between,
+    equals the eager result bit for bit."""
+    N, K = 256, 2048
+    w = rand_w(N, K, seed=77)
+    W = to_device(w, True)
+    codes, scales, _ = ssq.ssq_quantize(W, 32, 4, O.SIGNED_SYM)
+    x = to_device(synth.activations(M, K, seed=M), True)
+    y_eager = ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4)
+    y = torch.empty_like(y_eager)
+    ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4, out=y)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4, out=y)
+    for _ in range(4):
+        y.zero_()
+        graph.replay()
+        scratch = ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4)   # eager work between
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), y_eager.view(torch.int16))
+        assert torch.equal(scratch.view(torch.int16), y_eager.view(torch.int16))
+
+
 # ---------------------------------------------------------------------------
 # Full-size workloads (sampled output columns).
 # ---------------------------------------------------------------------------
