@@ -85,7 +85,8 @@ def parse_args():
     p.add_argument("--mode", choices=["signed_sym", "unsigned_sym", "asym"], default="signed_sym")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--phases", default="quantize,gemv,gemm",
-                   help="comma list of phases to run (profiling runs isolate one kernel)")
+                   help="comma list of phases to run (profiling runs isolate one kernel); "
+                        "'copy' adds a plain 256 MiB device copy used to calibrate byte counters")
     return p.parse_args()
 
 
@@ -205,7 +206,14 @@ def main() -> int:
         phases.update(saved)
     torch.cuda.synchronize()
 
+    copy_src = copy_dst = None
+    if "copy" in phases:    # plain copy of known size: the reference for HBM byte counters
+        copy_src = torch.ones(64 << 20, dtype=torch.int32, device=dev)
+        copy_dst = torch.empty_like(copy_src)
+
     def step(i, ev=None):
+        if copy_src is not None:
+            copy_dst.copy_(copy_src)
         if ev:
             ev[0].record()
         if "quantize" in phases:

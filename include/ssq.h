@@ -114,7 +114,7 @@ int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int 
  *   scales device, u16 [N, K/group]
  *   zp     device, u8 [N, K/group] for the asymmetric format, else NULL
  *   N      >= 0, number of weight rows (outputs)
- *   K      > 0, multiple of group
+ *   K      > 0, multiple of group, at most 2^23
  *   group  32, 64 or 128;  q  2, 3 or 4
  *   y      device, bf16 bits [M, N] row-major, written
  *   stream HIP stream the kernels are enqueued on (NULL: null stream)

@@ -3,14 +3,17 @@
 // App. B.3 of the paper: What[n,k] = s[n,b] (u[n,k] - o[n,b]).  Prefill is a
 // dense contraction, so it runs on bf16 MFMA.  Each workgroup owns a BM x BN
 // output tile; per BK-deep step it stages the activation tile and dequantizes
-// the weight tile (s*(u - o) is exact in fp32, then rounded to bf16) into LDS,
-// and each of its four wavefronts multiplies a 64x64 sub-tile with
-// v_mfma_f32_16x16x32_bf16, accumulating in fp32.
+// the weight tile (s*(u - o) is exact in fp32, then rounded to bf16) into one of
+// two LDS buffers while its four wavefronts multiply the other buffer's 64x64
+// sub-tiles with v_mfma_f32_16x16x32_bf16 (fp32 accumulation).  The next step's
+// global loads are issued before the current step's MFMAs; one barrier per step.
 //
 // MFMA operand layout (16x16x32): lane l supplies row (l % 16) of A and column
 // (l % 16) of B, each with 8 consecutive k values starting at 8 * (l / 16).
 // Both operands use the same k assignment, so the reduction is correct for any
 // internal k order.  Lane l receives D[4 * (l / 16) + r][l % 16], r = 0..3.
+#include <type_traits>
+
 #include "ssq_internal.h"
 
 namespace ssq {
@@ -21,11 +24,63 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int kStride = BK + 8;   // LDS row pitch in bf16 elements (144 bytes, 16-byte aligned)
+constexpr int kTileBytes = BM * BK * 2;     // one 128 x 64 bf16 tile: 128 rows of 128 bytes
+constexpr int kAStages = 3, kBStages = 2;   // 80 KB of LDS: two workgroups per CU
+
+// Byte offset of 16-byte chunk c (8 bf16 along k) of row r in a tile.  The chunk index
+// is XOR-swizzled with the row, so the 16 rows an MFMA operand read touches at one k
+// offset fall in 8 different chunk columns (no padding needed).
+__device__ __forceinline__ uint32_t swz(int r, int c) { return (uint32_t)(r * 128 + ((c ^ (r & 7)) << 4)); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   const bf16x2 v = {(__bf16)a, (__bf16)b};
   return __builtin_bit_cast(uint32_t, v);
+}
+
+// 32 weights s*(u - o) of one block as 16 bf16 pairs.  s*(u - o) is exact in fp32 (an
+// 11-bit scale times an integer below 2^5) and is rounded to bf16 once.
+template <int Q>
+__device__ __forceinline__ void dequant_block(const uint32_t (&d)[Q], float s, float so, uint32_t (&w)[16]) {
+  if constexpr (Q == 4) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t lo = d[i] & 0x0F0F0F0Fu, hi = (d[i] >> 4) & 0x0F0F0F0Fu;   // u[2b], u[2b+1]
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const float u0 = (float)((lo >> (8 * b)) & 0xFFu), u1 = (float)((hi >> (8 * b)) & 0xFFu);
+        w[4 * i + b] = pack_bf16x2(__builtin_fmaf(u0, s, so), __builtin_fmaf(u1, s, so));
+      }
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      w[k] = pack_bf16x2(__builtin_fmaf((float)field<Q>(d, 2 * k), s, so),
+                         __builtin_fmaf((float)field<Q>(d, 2 * k + 1), s, so));
+  }
+}
+
+// Tile order: workgroups are dealt round-robin to the 8 XCDs.  When the tile count
+// divides evenly, XCD x takes a contiguous run of tiles enumerated weight-panel
+// major (all M tiles of one N tile together), so a weight panel's codes are fetched
+// once per XCD and shared through its L2.
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn) {
+  const int total = tiles_m * tiles_n;
+  int t = (int)blockIdx.x;
+  if (total % 8 == 0) t = (t % 8) * (total / 8) + t / 8;
+  tn = t / tiles_m;
+  tm = t % tiles_m;
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// s_waitcnt on the vector-memory counter only (gfx9 encoding: vmcnt in bits 3:0 and
+// 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).  Loads complete in order,
+// so vmcnt <= N means everything but the last N loads has landed -- including loads
+// that write LDS directly, which the compiler does not track.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | 0x70 | 0xF00 | ((N >> 4) << 14));
 }
 
 template <int Q, int G, bool ZP>
@@ -34,19 +89,76 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
                                                    const uint16_t* __restrict__ scales,
                                                    const uint8_t* __restrict__ zp, int N, int K,
                                                    uint16_t* __restrict__ y) {
-  __shared__ __attribute__((aligned(16))) uint16_t As[BM * kStride];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[BN * kStride];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[(kAStages + kBStages) * kTileBytes];
+  uint8_t* const As = smem;
+  uint8_t* const Bs = smem + kAStages * kTileBytes;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
+  int tm, tn;
+  tile_of((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int nblk = K / 32;
-  const int64_t row_bytes = (int64_t)K * Q / 8;
-  const int groups_per_row = K / G;
+  const int nsteps = (nblk + 1) / 2;
+  const uint32_t row_bytes = (uint32_t)K * Q / 8;
+  const uint32_t groups_per_row = (uint32_t)(K / G);
+  constexpr float kSymOffset = (float)(1 << (Q - 1));
+  constexpr int kLoadsPerStep = 4 + 2 + (ZP ? 1 : 0);
 
-  // Loader roles: thread t stages row (t / 2), 32-wide half (t % 2) of both tiles.
+  // Buffer descriptors relative to the tile's first row; rows past M or N read zeros.
+  const uint32_t rows_a = (uint32_t)(M - m0 < BM ? M - m0 : BM);
+  const uint32_t rows_b = (uint32_t)(N - n0 < BN ? N - n0 : BN);
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(x + m0 * K, rows_a * (uint32_t)K * 2);
+  const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + n0 * row_bytes, rows_b * row_bytes);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + n0 * groups_per_row, rows_b * groups_per_row * 2);
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + n0 * groups_per_row : zp, ZP ? rows_b * groups_per_row : 0);
+
+  // Activation tile: 16 wavefront loads of 1 KB straight into LDS.  Wave w issues loads
+  // 4w..4w+3; load j fills tile rows 8j..8j+7, lane i writing 16 bytes at 16*i, which
+  // is row 8j + i/8, swizzled chunk i%8 -- so lane i fetches logical chunk (i%8)^(row%8).
+  uint32_t a_off[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = 8 * (4 * wave + j) + (lane >> 3);
+    const int c = (lane & 7) ^ (r & 7);
+    a_off[j] = (uint32_t)r * K * 2 + c * 16;
+  }
+  auto issue_a = [&](int step, int stage) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = (lane & 7) ^ ((8 * (4 * wave + j) + (lane >> 3)) & 7);
+      // chunks past K (odd block count, last step) read out of range -> zeros
+      const uint32_t off = step * 64 + c * 8 < K ? a_off[j] + (uint32_t)step * 128 : 0x80000000u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          ra, (lds_ptr_t)(As + stage * kTileBytes + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
+    }
+  };
+
+  // Weight tile: thread t dequantizes 32-weight block (t % 2) of row t / 2.
   const int lr = tid >> 1, lh = tid & 1;
-  const int64_t am = m0 + lr, bn = n0 + lr;
+  const uint32_t c_off = (uint32_t)lr * row_bytes + lh * (4 * Q);
+  uint32_t c_reg[2][Q], s_reg[2], z_reg[2];
+  auto issue_b = [&](int step, int slot) {
+    const int blk = 2 * step + lh;
+    const bool in = blk < nblk;
+    uint32_t d[Q];
+    buffer_block_codes<Q>(rc, in ? c_off + (uint32_t)step * (8 * Q) : 0x80000000u, 0, d);
+#pragma unroll
+    for (int i = 0; i < Q; ++i) c_reg[slot][i] = d[i];
+    const uint32_t gi = (uint32_t)lr * groups_per_row + (uint32_t)(blk / (G / 32));
+    s_reg[slot] = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? gi * 2 : 0x80000000u, 0, 0);
+    if constexpr (ZP) z_reg[slot] = __builtin_amdgcn_raw_buffer_load_b8(rz, in ? gi : 0x80000000u, 0, 0);
+  };
+  auto store_b = [&](int slot, int stage) {
+    const float s = f16_bits_to_f32(s_reg[slot]);
+    const float o = ZP ? (float)z_reg[slot] : kSymOffset;
+    uint32_t w[16];
+    dequant_block<Q>(c_reg[slot], s, -s * o, w);   // s*o is exact: o has at most 4 bits
+    uint8_t* dst = Bs + stage * kTileBytes;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      *reinterpret_cast<uint4*>(dst + swz(lr, lh * 4 + e)) = uint4{w[4 * e], w[4 * e + 1], w[4 * e + 2], w[4 * e + 3]};
+  };
 
   f32x4 acc[4][4];
 #pragma unroll
@@ -54,54 +166,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  for (int kb = 0; kb < nblk; kb += 2) {
-    const int blk = kb + lh;
-    // Activation tile: 32 bf16 (64 bytes) per thread.
-    {
-      uint4 v[4];
-      if (am < M && blk < nblk) {
-        const uint4* p = reinterpret_cast<const uint4*>(x + am * K + (int64_t)blk * 32);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = p[i];
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = uint4{0u, 0u, 0u, 0u};
-      }
-      uint4* dst = reinterpret_cast<uint4*>(As + lr * kStride + lh * 32);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dst[i] = v[i];
-    }
-    // Weight tile: dequantize one 32-weight block per thread.
-    {
-      uint32_t w[16];
-      if (bn < N && blk < nblk) {
-        uint32_t d[Q];
-        load_block_codes<Q>(codes + bn * row_bytes + (int64_t)blk * (4 * Q), d);
-        const int64_t gi = bn * groups_per_row + blk / (G / 32);
-        const float s = f16_bits_to_f32(scales[gi]);
-        const float o = ZP ? (float)zp[gi] : (float)(1 << (Q - 1));
-        const float so = -s * o;   // exact: o has at most 4 bits, s 11
-#pragma unroll
-        for (int k = 0; k < 16; ++k)
-          w[k] = pack_bf16x2(__builtin_fmaf((float)field<Q>(d, 2 * k), s, so),
-                             __builtin_fmaf((float)field<Q>(d, 2 * k + 1), s, so));
-      } else {
-#pragma unroll
-        for (int k = 0; k < 16; ++k) w[k] = 0u;
-      }
-      uint4* dst = reinterpret_cast<uint4*>(Bs + lr * kStride + lh * 32);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) dst[i] = uint4{w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]};
-    }
-    __syncthreads();
+  auto mfma_step = [&](int step) {
+    const uint8_t* at = As + (step % kAStages) * kTileBytes;
+    const uint8_t* bt = Bs + (step % kBStages) * kTileBytes;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 a[4], b[4];
-      const int kofs = ks * 32 + (lane >> 4) * 8;
+      const int c = ks * 4 + (lane >> 4);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        a[i] = *reinterpret_cast<const bf16x8*>(As + (wm * 64 + i * 16 + (lane & 15)) * kStride + kofs);
-        b[i] = *reinterpret_cast<const bf16x8*>(Bs + (wn * 64 + i * 16 + (lane & 15)) * kStride + kofs);
+        a[i] = *reinterpret_cast<const bf16x8*>(at + swz(wm * 64 + i * 16 + (lane & 15), c));
+        b[i] = *reinterpret_cast<const bf16x8*>(bt + swz(wn * 64 + i * 16 + (lane & 15), c));
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -109,7 +184,38 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
         for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
+  };
+
+  // Step s: issue loads for s+2, multiply stage s, dequantize codes of s+1, then wait
+  // for this wave's activation loads of s+1 and barrier.  Slots are static (the loop is
+  // unrolled by two) so the code registers never need dynamic indexing.
+  auto step_body = [&](int s, auto slot_c) {
+    constexpr int kSlot = decltype(slot_c)::value;
+    const bool ahead = s + 2 < nsteps;
+    if (ahead) {
+      issue_a(s + 2, (s + 2) % kAStages);
+      issue_b(s + 2, kSlot);
+    }
+    mfma_step(s);
+    if (s + 1 < nsteps) store_b(1 - kSlot, (s + 1) % kBStages);
+    if (ahead) wait_vmcnt<kLoadsPerStep>();
+    else wait_vmcnt<0>();
     __syncthreads();
+  };
+
+  issue_a(0, 0);
+  issue_b(0, 0);
+  if (nsteps > 1) {
+    issue_a(1, 1);
+    issue_b(1, 1);
+  }
+  store_b(0, 0);
+  if (nsteps > 1) wait_vmcnt<kLoadsPerStep>();
+  else wait_vmcnt<0>();
+  __syncthreads();
+  for (int s = 0; s < nsteps; s += 2) {
+    step_body(s, std::integral_constant<int, 0>{});
+    if (s + 1 < nsteps) step_body(s + 1, std::integral_constant<int, 1>{});
   }
 
 #pragma unroll
@@ -127,8 +233,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
 template <int Q, int G, bool ZP>
 hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                          const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
-  const dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
-  gemm_kernel<Q, G, ZP><<<grid, 256, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  gemm_kernel<Q, G, ZP><<<dim3((unsigned)tiles), 256, 0, stream>>>(x, (int)M, codes, scales, zp,
+                                                                     (int)N, (int)K, y);
   return hipGetLastError();
 }
 

@@ -10,6 +10,7 @@ namespace {
 
 constexpr int64_t kMaxElems = int64_t(1) << 40;   // rows*cols or N*K
 constexpr int64_t kMaxDim = int64_t(1) << 30;     // any single dimension (kernels index in int)
+constexpr int64_t kMaxK = int64_t(1) << 23;       // matmul reduction length (32-bit tile offsets)
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 bool valid_q(int q) { return q == 2 || q == 3 || q == 4; }
@@ -32,7 +33,7 @@ int check_quantize(const void* W, int64_t rows, int64_t cols, int group, int q, 
 
 int check_matmul(const void* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                  int64_t N, int64_t K, int group, int q, const void* y) {
-  if (M < 0 || N < 0 || K <= 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return SSQ_EINVAL;
+  if (M < 0 || N < 0 || K <= 0 || M > kMaxDim || N > kMaxDim || K > kMaxK) return SSQ_EINVAL;
   if (!valid_q(q) || !valid_group(group) || K % group != 0) return SSQ_EINVAL;
   if (N * K > kMaxElems || M * K > kMaxElems || M * N > kMaxElems) return SSQ_EINVAL;
   if (M == 0 || N == 0) return SSQ_OK;

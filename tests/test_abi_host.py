@@ -66,7 +66,8 @@ def test_quantize_empty_is_a_noop():
 
 
 @pytest.mark.parametrize("args", [
-    dict(K=0), dict(K=48), dict(K=-32), dict(M=-1), dict(N=-1), dict(q=8), dict(group=96),
+    dict(K=0), dict(K=48), dict(K=-32), dict(K=(1 << 23) + 32), dict(M=-1), dict(N=-1), dict(q=8),
+    dict(group=96),
     dict(x=None), dict(codes=None), dict(scales=None), dict(y=None),
 ])
 def test_matmul_rejects_invalid_arguments(args):
