@@ -174,6 +174,8 @@ def main() -> int:
     staging = ssq.ssq_quantize(W, g, q, mode)                      # quantize target each step
     y1 = torch.empty((1, N), dtype=torch.bfloat16, device=dev)
     ym = torch.empty((args.gemm_m, N), dtype=torch.bfloat16, device=dev)
+    # the prefill GEMM gets the split-reduction workspace it asks for (None: no split)
+    gemm_ws = ssq.ssq_matmul_workspace(args.gemm_m, N, K, g, q, device=dev)
     torch.cuda.synchronize()
 
     # The decode GEMVs and prefill GEMMs of one step are captured once in a HIP graph
@@ -188,7 +190,7 @@ def main() -> int:
         if "gemm" in phases:
             for r in range(args.gemm_layers):
                 c, s, z = layers[(i * args.gemm_layers + r) % args.layers]
-                ssq.ssq_matmul(xm, c, s, z, N, K, g, q, out=ym)
+                ssq.ssq_matmul(xm, c, s, z, N, K, g, q, out=ym, workspace=gemm_ws)
 
     graphs = {}
     for part in ("gemv", "gemm"):
@@ -268,6 +270,7 @@ def main() -> int:
         "config": {"workload": "llama3_8b_down_proj_4096x14336_w4g32", "N": N, "K": K, "q": q,
                    "group": g, "mode": args.mode, "decode_M": 1, "decode_layers": args.layers,
                    "prefill_M": args.gemm_m, "prefill_layers": args.gemm_layers,
+                   "prefill_workspace_bytes": 0 if gemm_ws is None else gemm_ws.numel(),
                    "weights": f"bf16 Student-t(5)*0.02 + 0.1% x20 outliers, seed {spec.seed}"},
         "wall_s": round(wall, 4),
     }

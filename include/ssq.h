@@ -27,7 +27,8 @@
  *
  * Conventions
  *   - Every pointer is a device pointer owned by the caller.  The library
- *     allocates nothing, frees nothing and keeps no pointer after returning.
+ *     allocates nothing, frees nothing and keeps no pointer after returning;
+ *     scratch memory, where a path can use it, is a caller-provided workspace.
  *   - W, x, y and codes must be 16-byte aligned; scales 2-byte aligned.
  *   - bf16 and fp16 tensors are passed as their uint16_t bit patterns.
  *   - Inputs must be finite; NaN/Inf inputs give unspecified codes.
@@ -41,6 +42,7 @@
 #ifndef SSQ_H
 #define SSQ_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -122,6 +124,33 @@ int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int 
 int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
                hipStream_t stream);
+
+/*
+ * ssq_matmul_workspace_size -- bytes of workspace that let ssq_matmul_ws split
+ * the reduction of an M x N x K product across workgroups (App. B.3 sums over
+ * blocks of K, so disjoint block ranges can be reduced separately and added).
+ * Returns 0 when splitting would not help (enough output tiles already, M < 2)
+ * or the arguments are invalid.
+ */
+size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q);
+
+/*
+ * ssq_matmul_ws -- ssq_matmul with a caller-provided device workspace.  With a
+ * workspace of at least ssq_matmul_workspace_size() bytes the GEMM splits its
+ * reduction; with a smaller one, or NULL, it behaves exactly like ssq_matmul.
+ *   workspace       device, 256-byte aligned, zero-filled by the caller before
+ *                   its first use; every call leaves it reusable (the arrival
+ *                   counters it holds return to zero).  Two calls that may run
+ *                   concurrently must not share a workspace.
+ *   workspace_bytes size of the workspace in bytes
+ * Other arguments, results and errors as ssq_matmul (plus SSQ_EALIGN for a
+ * misaligned workspace).  The split adds fp32 partials in a fixed order, so
+ * results are reproducible, but y can differ from ssq_matmul's in the last
+ * bf16 bit (a different summation order).
+ */
+int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                  const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ssq_matmul with binary32 x[M, K] and y[M, N] (fp32 accumulation and output). */
 int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,

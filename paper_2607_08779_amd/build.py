@@ -22,6 +22,7 @@ ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-ffp-contract=off",                      # every fma in the kernels is written out
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",     # MFMA accumulators in VGPRs: no AGPR copies in loops
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}",
 ]

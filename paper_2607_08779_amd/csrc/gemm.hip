@@ -12,6 +12,7 @@
 // (l % 16) of B, each with 8 consecutive k values starting at 8 * (l / 16).
 // Both operands use the same k assignment, so the reduction is correct for any
 // internal k order.  Lane l receives D[4 * (l / 16) + r][l % 16], r = 0..3.
+#include <algorithm>
 #include <type_traits>
 
 #include "ssq_internal.h"
@@ -37,41 +38,102 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// 32 weights s*(u - o) of one block as 16 bf16 pairs.  s*(u - o) is exact in fp32 (an
-// 11-bit scale times an integer below 2^5) and is rounded to bf16 once.
+__device__ __forceinline__ float f16_lo(uint32_t p) { return (float)__builtin_bit_cast(_Float16, (uint16_t)p); }
+__device__ __forceinline__ float f16_hi(uint32_t p) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(p >> 16)); }
+
+// 32 weights s*(u - o) of one block as 16 bf16 pairs (natural k order).  Each q-bit
+// field is OR-ed into the mantissa of the fp16 constant 1024 (0x6400 | u == 1024 + u),
+// two fields per instruction; one v_fma_mix_f32 per weight then forms
+// (1024 + u)*s - (1024 + o)*s.  Both products are exact in fp32 (11-bit by 11-bit), so
+// the result is s*(u - o) exactly; it is rounded to bf16 once.  `so` = -(1024 + o)*s.
 template <int Q>
 __device__ __forceinline__ void dequant_block(const uint32_t (&d)[Q], float s, float so, uint32_t (&w)[16]) {
+  const uint32_t magic = 0x64006400u;
+  float f[32];
   if constexpr (Q == 4) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const uint32_t lo = d[i] & 0x0F0F0F0Fu, hi = (d[i] >> 4) & 0x0F0F0F0Fu;   // u[2b], u[2b+1]
+      const uint32_t v4 = d[i] >> 4;
+      const uint32_t p[4] = {and_or(d[i], 0x000F000Fu, magic), and_or(v4, 0x000F000Fu, magic),
+                             and_or(d[i] >> 8, 0x000F000Fu, magic), and_or(v4 >> 8, 0x000F000Fu, magic)};
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const float u0 = (float)((lo >> (8 * b)) & 0xFFu), u1 = (float)((hi >> (8 * b)) & 0xFFu);
-        w[4 * i + b] = pack_bf16x2(__builtin_fmaf(u0, s, so), __builtin_fmaf(u1, s, so));
+      for (int j = 0; j < 4; ++j) {          // p[j] holds fields j and j + 4 of this dword
+        f[8 * i + j] = __builtin_fmaf(f16_lo(p[j]), s, so);
+        f[8 * i + j + 4] = __builtin_fmaf(f16_hi(p[j]), s, so);
       }
     }
-  } else {
+  } else if constexpr (Q == 2) {
 #pragma unroll
-    for (int k = 0; k < 16; ++k)
-      w[k] = pack_bf16x2(__builtin_fmaf((float)field<Q>(d, 2 * k), s, so),
-                         __builtin_fmaf((float)field<Q>(d, 2 * k + 1), s, so));
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {          // fields j and j + 8 of this dword
+        const uint32_t p = and_or(d[i] >> (2 * j), 0x00030003u, magic);
+        f[16 * i + j] = __builtin_fmaf(f16_lo(p), s, so);
+        f[16 * i + j + 8] = __builtin_fmaf(f16_hi(p), s, so);
+      }
+  } else {
+    // Four 24-bit words of 8 fields; fields 4..7 of each word moved up to bit 16.
+    const uint32_t v[4] = {d[0], __builtin_amdgcn_alignbit(d[1], d[0], 24),
+                           __builtin_amdgcn_alignbit(d[2], d[1], 16), d[2] >> 8};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t sp = (v[i] & 0xFFFu) | ((v[i] << 4) & 0x0FFF0000u);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t p = and_or(sp >> (3 * j), 0x00070007u, magic);
+        f[8 * i + j] = __builtin_fmaf(f16_lo(p), s, so);
+        f[8 * i + j + 4] = __builtin_fmaf(f16_hi(p), s, so);
+      }
+    }
   }
+#pragma unroll
+  for (int k = 0; k < 16; ++k) w[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
 }
 
 // Tile order: workgroups are dealt round-robin to the 8 XCDs.  When the tile count
 // divides evenly, XCD x takes a contiguous run of tiles enumerated weight-panel
 // major (all M tiles of one N tile together), so a weight panel's codes are fetched
 // once per XCD and shared through its L2.
-__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tm, int& tn) {
+__device__ __forceinline__ void tile_of(int t, int tiles_m, int tiles_n, int& tm, int& tn) {
   const int total = tiles_m * tiles_n;
-  int t = (int)blockIdx.x;
   if (total % 8 == 0) t = (t % 8) * (total / 8) + t / 8;
   tn = t / tiles_m;
   tm = t % tiles_m;
 }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// ---------------------------------------------------------------------------
+// Split reduction (host side).  When the output has too few tiles to occupy the CUs
+// twice over, the K steps of each tile are divided among `splits` workgroups whose fp32
+// partial tiles meet in a caller-provided workspace: [counters: one u32 per tile,
+// padded to 256 bytes][partials: tiles x splits x BM x BN fp32].
+// ---------------------------------------------------------------------------
+constexpr int64_t kTargetWorkgroups = 512;   // two resident workgroups per CU
+constexpr int kMinStepsPerSplit = 16;
+
+int64_t counter_bytes(int64_t tiles) { return (tiles * 4 + 255) / 256 * 256; }
+
+int desired_splits(int64_t M, int64_t N, int64_t K) {
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  const int64_t steps = (K / 32 + 1) / 2;
+  int64_t s = kTargetWorkgroups / tiles;
+  s = std::min<int64_t>(s, steps / kMinStepsPerSplit);
+  s = std::min<int64_t>(s, 8);
+  return (int)std::max<int64_t>(s, 1);
+}
+
+int64_t workspace_for(int64_t M, int64_t N, int64_t K, int splits) {
+  if (splits <= 1) return 0;
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  return counter_bytes(tiles) + tiles * splits * BM * BN * 4;
+}
+
+int gemm_splits(int64_t M, int64_t N, int64_t K, const void* workspace, size_t bytes) {
+  const int s = desired_splits(M, N, K);
+  if (s <= 1 || workspace == nullptr || (int64_t)bytes < workspace_for(M, N, K, s)) return 1;
+  return s;
+}
 
 // s_waitcnt on the vector-memory counter only (gfx9 encoding: vmcnt in bits 3:0 and
 // 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).  Loads complete in order,
@@ -88,18 +150,28 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
                                                    const uint8_t* __restrict__ codes,
                                                    const uint16_t* __restrict__ scales,
                                                    const uint8_t* __restrict__ zp, int N, int K,
-                                                   uint16_t* __restrict__ y) {
+                                                   uint16_t* __restrict__ y, int splits,
+                                                   float* __restrict__ partials,
+                                                   unsigned int* __restrict__ counters) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[(kAStages + kBStages) * kTileBytes];
   uint8_t* const As = smem;
   uint8_t* const Bs = smem + kAStages * kTileBytes;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+  const int tiles = tiles_m * tiles_n;
+  const int tile_id = (int)blockIdx.x % tiles;   // splits of one tile share no operand data
+  const int split = (int)blockIdx.x / tiles;
   int tm, tn;
-  tile_of((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  tile_of(tile_id, tiles_m, tiles_n, tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int nblk = K / 32;
-  const int nsteps = (nblk + 1) / 2;
+  const int total_steps = (nblk + 1) / 2;
+  // This workgroup's slice of the reduction: steps [s_begin, s_begin + nsteps).
+  const int per_split = (total_steps + splits - 1) / splits;
+  const int s_begin = split * per_split;
+  const int nsteps = total_steps - s_begin < per_split ? total_steps - s_begin : per_split;
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
   const uint32_t groups_per_row = (uint32_t)(K / G);
   constexpr float kSymOffset = (float)(1 << (Q - 1));
@@ -123,7 +195,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     const int c = (lane & 7) ^ (r & 7);
     a_off[j] = (uint32_t)r * K * 2 + c * 16;
   }
-  auto issue_a = [&](int step, int stage) {
+  auto issue_a = [&](int lstep, int stage) {
+    const int step = s_begin + lstep;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c = (lane & 7) ^ ((8 * (4 * wave + j) + (lane >> 3)) & 7);
@@ -138,7 +211,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
   const int lr = tid >> 1, lh = tid & 1;
   const uint32_t c_off = (uint32_t)lr * row_bytes + lh * (4 * Q);
   uint32_t c_reg[2][Q], s_reg[2], z_reg[2];
-  auto issue_b = [&](int step, int slot) {
+  auto issue_b = [&](int lstep, int slot) {
+    const int step = s_begin + lstep;
     const int blk = 2 * step + lh;
     const bool in = blk < nblk;
     uint32_t d[Q];
@@ -153,7 +227,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     const float s = f16_bits_to_f32(s_reg[slot]);
     const float o = ZP ? (float)z_reg[slot] : kSymOffset;
     uint32_t w[16];
-    dequant_block<Q>(c_reg[slot], s, -s * o, w);   // s*o is exact: o has at most 4 bits
+    dequant_block<Q>(c_reg[slot], s, -(1024.0f + o) * s, w);   // exact: 11-bit times 11-bit
     uint8_t* dst = Bs + stage * kTileBytes;
 #pragma unroll
     for (int e = 0; e < 4; ++e)
@@ -218,6 +292,45 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     if (s + 1 < nsteps) step_body(s + 1, std::integral_constant<int, 1>{});
   }
 
+  if (splits > 1) {
+    // Split reduction: publish this slice's fp32 partial tile in the lane order of the
+    // accumulators (coalesced), then count arrivals; the last arriving workgroup sums
+    // all slices in a fixed order, writes y and resets the counter so the workspace
+    // stays reusable.
+    float* mine = partials + ((int64_t)tile_id * splits + split) * (BM * BN) + wave * 4096 + lane;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mine[((i * 4 + j) * 4 + r) * 64] = acc[i][j][r];
+    __threadfence();                       // release the partial to the whole device
+    // The tile buffers are idle after the main loop; their first word carries the arrival
+    // count to the whole workgroup (a separate shared variable would push LDS past 80 KB
+    // and halve the workgroups per CU).
+    unsigned int* arrived = reinterpret_cast<unsigned int*>(smem);
+    __syncthreads();
+    if (tid == 0) *arrived = atomicAdd(&counters[tile_id], 1u);
+    __syncthreads();
+    if (*arrived != (unsigned int)(splits - 1)) return;   // uniform across the workgroup
+    __threadfence();                       // acquire the other slices' partials
+    // Sum every slice (this one included) in slice order, so the result does not depend
+    // on which workgroup arrived last.
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int o = 0; o < splits; ++o) {
+      const float* part = partials + ((int64_t)tile_id * splits + o) * (BM * BN) + wave * 4096 + lane;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc[i][j][r] += __builtin_nontemporal_load(part + ((i * 4 + j) * 4 + r) * 64);
+    }
+    if (tid == 0) counters[tile_id] = 0u;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -232,10 +345,15 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
 
 template <int Q, int G, bool ZP>
 hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
-                         const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+                         const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
   const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  gemm_kernel<Q, G, ZP><<<dim3((unsigned)tiles), 256, 0, stream>>>(x, (int)M, codes, scales, zp,
-                                                                     (int)N, (int)K, y);
+  const int splits = gemm_splits(M, N, K, workspace, workspace_bytes);
+  unsigned int* counters = static_cast<unsigned int*>(workspace);
+  float* partials = splits > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + counter_bytes(tiles))
+                               : nullptr;
+  gemm_kernel<Q, G, ZP><<<dim3((unsigned)(tiles * splits)), 256, 0, stream>>>(
+      x, (int)M, codes, scales, zp, (int)N, (int)K, y, splits, partials, counters);
   return hipGetLastError();
 }
 
@@ -243,8 +361,14 @@ hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, con
 
 hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
                             const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
-                            int group, int q, uint16_t* y, hipStream_t stream) {
-  SSQ_DISPATCH_QGZ(gemm_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y, stream);
+                            int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+  SSQ_DISPATCH_QGZ(gemm_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y,
+                   workspace, workspace_bytes, stream);
+}
+
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  return (size_t)workspace_for(M, N, K, desired_splits(M, N, K));
 }
 
 }  // namespace ssq

@@ -31,11 +31,16 @@ int check_quantize(const void* W, int64_t rows, int64_t cols, int group, int q, 
   return SSQ_OK;
 }
 
-int check_matmul(const void* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
-                 int64_t N, int64_t K, int group, int q, const void* y) {
+int check_matmul_sizes(int64_t M, int64_t N, int64_t K, int group, int q) {
   if (M < 0 || N < 0 || K <= 0 || M > kMaxDim || N > kMaxDim || K > kMaxK) return SSQ_EINVAL;
   if (!valid_q(q) || !valid_group(group) || K % group != 0) return SSQ_EINVAL;
   if (N * K > kMaxElems || M * K > kMaxElems || M * N > kMaxElems) return SSQ_EINVAL;
+  return SSQ_OK;
+}
+
+int check_matmul(const void* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                 int64_t N, int64_t K, int group, int q, const void* y) {
+  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK) return SSQ_EINVAL;
   if (M == 0 || N == 0) return SSQ_OK;
   if (x == nullptr || codes == nullptr || scales == nullptr || y == nullptr) return SSQ_EINVAL;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(y, 16) || !aligned(scales, 2))
@@ -67,7 +72,23 @@ int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_
   const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
   if (st != SSQ_OK || M == 0 || N == 0) return st;
   if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
-  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, stream));
+  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, nullptr, 0, stream));
+}
+
+size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q) {
+  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M < 2 || N == 0) return 0;
+  return ssq::gemm_workspace_bytes(M, N, K);
+}
+
+int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                  const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  if (workspace != nullptr && !aligned(workspace, 256)) return SSQ_EALIGN;
+  if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
+  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace,
+                                         workspace_bytes, stream));
 }
 
 int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
@@ -82,7 +103,7 @@ const char* ssq_strerror(int status) {
   switch (status) {
     case SSQ_OK: return "success";
     case SSQ_EINVAL: return "invalid argument (size, q, group, mode or zero-point/mode mismatch)";
-    case SSQ_EALIGN: return "misaligned pointer (W, x, y, codes need 16 bytes; scales 2)";
+    case SSQ_EALIGN: return "misaligned pointer (W, x, y, codes need 16 bytes; scales 2; workspace 256)";
     case SSQ_EHIP: return "HIP runtime error at kernel launch";
     default: return "unknown status";
   }

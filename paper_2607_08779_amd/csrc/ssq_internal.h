@@ -170,6 +170,9 @@ hipError_t launch_matmul_f32(const float* x, int64_t M, const uint8_t* codes,
                              int group, int q, float* y, hipStream_t stream);
 hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
                             const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
-                            int group, int q, uint16_t* y, hipStream_t stream);
+                            int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream);
+// Workspace bytes that let the GEMM split its reduction (0 when splitting would not help).
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 }  // namespace ssq

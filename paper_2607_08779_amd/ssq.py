@@ -32,6 +32,12 @@ _EXPORTS = {
                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                       ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                       ctypes.c_void_p]),
+    "ssq_matmul_workspace_size": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                                     ctypes.c_int, ctypes.c_int]),
+    "ssq_matmul_ws": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                     ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.c_size_t, ctypes.c_void_p]),
     "ssq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
 }
 
@@ -107,12 +113,26 @@ def ssq_quantize(W: torch.Tensor, group: int, q: int, mode: int,
     return codes, scales, zp
 
 
+def ssq_matmul_workspace_size(M: int, N: int, K: int, group: int, q: int) -> int:
+    """Bytes of workspace that let ssq_matmul_ws split the reduction (0: no benefit)."""
+    return int(lib().ssq_matmul_workspace_size(M, N, K, group, q))
+
+
+def ssq_matmul_workspace(M: int, N: int, K: int, group: int, q: int,
+                         device=None) -> Optional[torch.Tensor]:
+    """A zero-filled workspace tensor for ssq_matmul(..., workspace=...), or None."""
+    n = ssq_matmul_workspace_size(M, N, K, group, q)
+    return torch.zeros(n, dtype=torch.uint8, device=device or "cuda") if n else None
+
+
 def ssq_matmul(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
                zp: Optional[torch.Tensor], N: int, K: int, group: int, q: int,
-               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+               out: Optional[torch.Tensor] = None,
+               workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """y [M, N] = x [M, K] @ dequant(codes, scales, zp)^T on the current stream.
 
-    x bf16 gives y bf16 (``ssq_matmul``); x fp32 gives y fp32 (``ssq_matmul_f32``).
+    x bf16 gives y bf16 (``ssq_matmul``, or ``ssq_matmul_ws`` when a workspace is
+    given); x fp32 gives y fp32 (``ssq_matmul_f32``).
     """
     if x.dim() != 2 or not x.is_contiguous() or x.shape[1] != K:
         raise ValueError("x must be a contiguous [M, K] tensor")
@@ -124,7 +144,13 @@ def ssq_matmul(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
         raise TypeError("x must be bfloat16 or float32")
     M = x.shape[0]
     y = torch.empty((M, N), dtype=x.dtype, device=x.device) if out is None else out
-    st = getattr(lib(), fn)(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
-                            _ptr(y), _stream(x.device))
+    if workspace is not None and fn == "ssq_matmul":
+        fn = "ssq_matmul_ws"
+        st = lib().ssq_matmul_ws(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
+                                 _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 _stream(x.device))
+    else:
+        st = getattr(lib(), fn)(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
+                                _ptr(y), _stream(x.device))
     _check(fn, st)
     return y

@@ -23,8 +23,9 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_quantize",
-                                    "ssq_quantize_f32", "ssq_strerror"]
+    assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_matmul_workspace_size",
+                                    "ssq_matmul_ws", "ssq_quantize", "ssq_quantize_f32",
+                                    "ssq_strerror"]
 
 
 def test_library_exports_every_declared_symbol():
@@ -89,6 +90,23 @@ def test_matmul_rejects_misaligned_pointers(which):
 def test_matmul_empty_is_a_noop():
     for M, N in ((0, 8), (2, 0)):
         assert ssq.lib().ssq_matmul(None, M, None, None, None, N, 64, 32, 4, None, None) == 0
+
+
+def test_workspace_size_rules():
+    lib = ssq.lib()
+    # the headline prefill shape has 128 output tiles of 128x128: worth splitting 4 ways
+    n = lib.ssq_matmul_workspace_size(512, 4096, 14336, 32, 4)
+    assert n == 512 + 128 * 4 * 128 * 128 * 4          # counters (128 x u32) + partials
+    assert lib.ssq_matmul_workspace_size(2048, 14336, 4096, 32, 4) == 0   # enough tiles
+    assert lib.ssq_matmul_workspace_size(1, 4096, 14336, 32, 4) == 0      # GEMV never splits
+    assert lib.ssq_matmul_workspace_size(512, 4096, 48, 32, 4) == 0       # invalid K
+    assert lib.ssq_matmul_workspace_size(512, 4096, 256, 32, 4) == 0      # too few steps
+
+
+def test_matmul_ws_rejects_misaligned_workspace():
+    st = ssq.lib().ssq_matmul_ws(P16, 2, P16, P16, None, 8, 64, 32, 4, P16,
+                                 ctypes.c_void_p((1 << 20) + 16), 1 << 20, None)
+    assert st == EALIGN
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):

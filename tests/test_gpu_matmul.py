@@ -22,19 +22,29 @@ TOL_BF16 = 2e-2
 TOL_F32 = 1e-3
 
 
-def check_matmul(w_host, x_host, group, q, mode, rows_idx=None, bf16_w=True, bf16_x=True, tag=""):
-    """Quantize on the GPU, multiply on the GPU, compare with the oracle on rows_idx."""
+def check_matmul(w_host, x_host, group, q, mode, rows_idx=None, bf16_w=True, bf16_x=True, tag="",
+                 workspace=False, repeat=1):
+    """Quantize on the GPU, multiply on the GPU, compare with the oracle on rows_idx.
+    With workspace=True the split-reduction entry point runs `repeat` times on one
+    workspace and every result is checked."""
     N, K = w_host.shape
     W = to_device(w_host, bf16_w)
     codes, scales, zp = ssq.ssq_quantize(W, group, q, mode)
     X = to_device(x_host, bf16_x)
-    y = ssq.ssq_matmul(X, codes, scales, zp, N, K, group, q)
+    ws = ssq.ssq_matmul_workspace(x_host.shape[0], N, K, group, q) if workspace else None
+    if workspace:
+        assert ws is not None, "shape chosen to need a split"
+    ys = [ssq.ssq_matmul(X, codes, scales, zp, N, K, group, q, workspace=ws) for _ in range(repeat)]
+    y = ys[-1]
     torch.cuda.synchronize()
     sel = np.arange(N) if rows_idx is None else rows_idx
     ref_q = O.quantize(widen(w_host[sel], bf16_w), group, q, mode)
     assert_quant_equal((codes, scales, zp), ref_q, None if rows_idx is None else sel, tag=tag)
     xr = widen(x_host, bf16_x)
     y_ref = O.matmul(xr, ref_q.codes, ref_q.scales, ref_q.zp, len(sel), K, group, q)
+    for earlier in ys[:-1]:      # same workspace, same answer every call
+        err_rep = rel_l2(y_to_f64(earlier)[:, sel], y_ref)
+        assert err_rep <= (TOL_BF16 if bf16_x else TOL_F32), f"{tag}: repeated call rel L2 {err_rep:.3e}"
     y_gpu = y_to_f64(y)[:, sel]
     err = rel_l2(y_gpu, y_ref)
     M = x_host.shape[0]
@@ -92,6 +102,47 @@ def test_gemm_small_token_counts(M):
     w = rand_w(64, 512, seed=M)
     x = synth.activations(M, 512, seed=M)
     check_matmul(w, x, 32, 4, O.SIGNED_SYM, tag=f"gemm M={M}")
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("mode", MODES)
+def test_gemm_split_reduction_ragged(q, mode):
+    # 4 output tiles (130x200) over K=3104 (97 blocks, 49 steps): split 3 ways, the last
+    # slice carrying the odd half-step; three calls on one workspace
+    w = rand_w(200, 3104, seed=q + 10 * mode)
+    x = synth.activations(130, 3104, seed=q)
+    check_matmul(w, x, 32, q, mode, tag="split 130x200x3104", workspace=True, repeat=3)
+
+
+def test_gemm_split_reduction_eight_ways():
+    w = rand_w(160, 8192, seed=5)
+    x = synth.activations(64, 8192, seed=5)
+    check_matmul(w, x, 128, 4, O.SIGNED_SYM, tag="split 64x160x8192", workspace=True, repeat=2)
+
+
+def test_split_reduction_graph_replay():
+    """The split GEMM in a HIP graph: the arrival counters reset inside the kernel, so
+    every replay (with eager work between) reproduces the first result."""
+    M, N, K = 96, 256, 8192
+    W = to_device(rand_w(N, K, seed=8), True)
+    codes, scales, _ = ssq.ssq_quantize(W, 32, 4, O.SIGNED_SYM)
+    x = to_device(synth.activations(M, K, seed=8), True)
+    ws = ssq.ssq_matmul_workspace(M, N, K, 32, 4)
+    assert ws is not None
+    y_eager = ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4, workspace=ws)
+    y = torch.empty_like(y_eager)
+    ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4, out=y, workspace=ws)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4, out=y, workspace=ws)
+    for _ in range(4):
+        y.zero_()
+        graph.replay()
+        other = ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4)
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), y_eager.view(torch.int16))
+        assert rel_l2(y_to_f64(other), y_to_f64(y_eager)) < 1e-2
 
 
 @pytest.mark.parametrize("M", [1, 3, 5])
@@ -196,6 +247,16 @@ def test_prefill_gemm_full_size(M, layer):
     x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
     check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=32, seed=M),
                  tag=f"prefill {layer} M={M}")
+
+
+def test_prefill_headline_split_full_size():
+    """M=512 on the 4096x14336 down projection through the split-reduction entry point."""
+    wl = synth.prefill()
+    spec = wl.layers["down_proj"]
+    w = weights_host(spec)
+    x = synth.activations(512, spec.cols, seed=wl.x_seed + 512)
+    check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=32, seed=9),
+                 tag="prefill down_proj M=512 split", workspace=True, repeat=2)
 
 
 @pytest.mark.parametrize("M", [1, 16])
