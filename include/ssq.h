@@ -107,8 +107,9 @@ int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int 
  *   o = 2^(q-1) when zp == NULL (symmetric formats, signed or not: the sign
  *   lives in the scale, so both run the same kernel), o = zp[n, b] otherwise.
  * Products accumulate in fp32; y is rounded to bf16 (half to even).
- * M = 1 runs a streaming GEMV; larger M runs a tiled kernel that dequantizes
- * weight tiles into LDS and multiplies them with bf16 MFMA.
+ * M = 1 runs a streaming GEMV; 2 <= M <= 32 (batched decode) dequantizes each
+ * weight once into bf16 MFMA operands shared by all tokens; larger M runs a tiled
+ * kernel that dequantizes weight tiles into LDS and multiplies them with bf16 MFMA.
  *
  *   x      device, bf16 bits [M, K] row-major, read only
  *   M      >= 0, number of activation rows (tokens)
@@ -116,7 +117,7 @@ int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int 
  *   scales device, u16 [N, K/group]
  *   zp     device, u8 [N, K/group] for the asymmetric format, else NULL
  *   N      >= 0, number of weight rows (outputs)
- *   K      > 0, multiple of group, at most 2^23
+ *   K      > 0, multiple of group, at most 2^22
  *   group  32, 64 or 128;  q  2, 3 or 4
  *   y      device, bf16 bits [M, N] row-major, written
  *   stream HIP stream the kernels are enqueued on (NULL: null stream)
@@ -129,8 +130,8 @@ int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_
  * ssq_matmul_workspace_size -- bytes of workspace that let ssq_matmul_ws split
  * the reduction of an M x N x K product across workgroups (App. B.3 sums over
  * blocks of K, so disjoint block ranges can be reduced separately and added).
- * Returns 0 when splitting would not help (enough output tiles already, M < 2)
- * or the arguments are invalid.
+ * Returns 0 when splitting would not help (enough output tiles already, or
+ * M <= 32, which never uses the tiled kernel) or the arguments are invalid.
  */
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q);
 

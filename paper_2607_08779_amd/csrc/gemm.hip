@@ -1,12 +1,14 @@
 // Prefill GEMM: y[M,N] = x[M,K] * What[N,K]^T with What dequantized into LDS.
 //
 // App. B.3 of the paper: What[n,k] = s[n,b] (u[n,k] - o[n,b]).  Prefill is a
-// dense contraction, so it runs on bf16 MFMA.  Each workgroup owns a BM x BN
-// output tile; per BK-deep step it stages the activation tile and dequantizes
-// the weight tile (s*(u - o) is exact in fp32, then rounded to bf16) into one of
-// two LDS buffers while its four wavefronts multiply the other buffer's 64x64
-// sub-tiles with v_mfma_f32_16x16x32_bf16 (fp32 accumulation).  The next step's
-// global loads are issued before the current step's MFMAs; one barrier per step.
+// dense contraction, so it runs on bf16 MFMA.  A workgroup of 2*WM wavefronts owns
+// a (64*WM) x 128 output tile, each wavefront a 64x64 sub-tile of
+// v_mfma_f32_16x16x32_bf16 (fp32 accumulation).  Per 64-deep step the activation
+// tile streams from memory straight into an LDS ring (buffer_load ... lds, several
+// steps ahead), weight codes are prefetched into registers and dequantized one step
+// ahead (s*(u - o), exact in fp32, rounded to bf16) into a second LDS ring; one
+// barrier per step.  WM=4 uses the full 160 KB of LDS (one workgroup per CU, a
+// four-stage activation ring); WM=2 fits two workgroups per CU.
 //
 // MFMA operand layout (16x16x32): lane l supplies row (l % 16) of A and column
 // (l % 16) of B, each with 8 consecutive k values starting at 8 * (l / 16).
@@ -16,79 +18,33 @@
 #include <type_traits>
 
 #include "ssq_internal.h"
+#include "mfma_dequant.h"
 
 namespace ssq {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int kTileBytes = BM * BK * 2;     // one 128 x 64 bf16 tile: 128 rows of 128 bytes
-constexpr int kAStages = 3, kBStages = 2;   // 80 KB of LDS: two workgroups per CU
+constexpr int BN = 128, BK = 64;
+constexpr int kBTileBytes = BN * BK * 2;     // 16 KB: 128 rows of 128 bytes
+constexpr int kBStages = 2;
+
+template <int WM>
+struct Cfg {
+  static constexpr int BM = 64 * WM;                    // output rows per tile
+  static constexpr int kWaves = 2 * WM;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kAStages = WM == 2 ? 3 : 4;      // 80 KB or 160 KB of LDS in total
+  static constexpr int kAhead = kAStages - 1;           // steps of loads in flight
+  static constexpr int kATileBytes = BM * BK * 2;
+  static constexpr int kParts = kThreads / 256;         // threads per 32-weight block
+  static constexpr int kLds = kAStages * kATileBytes + kBStages * kBTileBytes;
+};
 
 // Byte offset of 16-byte chunk c (8 bf16 along k) of row r in a tile.  The chunk index
 // is XOR-swizzled with the row, so the 16 rows an MFMA operand read touches at one k
 // offset fall in 8 different chunk columns (no padding needed).
 __device__ __forceinline__ uint32_t swz(int r, int c) { return (uint32_t)(r * 128 + ((c ^ (r & 7)) << 4)); }
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  const bf16x2 v = {(__bf16)a, (__bf16)b};
-  return __builtin_bit_cast(uint32_t, v);
-}
-
-__device__ __forceinline__ float f16_lo(uint32_t p) { return (float)__builtin_bit_cast(_Float16, (uint16_t)p); }
-__device__ __forceinline__ float f16_hi(uint32_t p) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(p >> 16)); }
-
-// 32 weights s*(u - o) of one block as 16 bf16 pairs (natural k order).  Each q-bit
-// field is OR-ed into the mantissa of the fp16 constant 1024 (0x6400 | u == 1024 + u),
-// two fields per instruction; one v_fma_mix_f32 per weight then forms
-// (1024 + u)*s - (1024 + o)*s.  Both products are exact in fp32 (11-bit by 11-bit), so
-// the result is s*(u - o) exactly; it is rounded to bf16 once.  `so` = -(1024 + o)*s.
-template <int Q>
-__device__ __forceinline__ void dequant_block(const uint32_t (&d)[Q], float s, float so, uint32_t (&w)[16]) {
-  const uint32_t magic = 0x64006400u;
-  float f[32];
-  if constexpr (Q == 4) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t v4 = d[i] >> 4;
-      const uint32_t p[4] = {and_or(d[i], 0x000F000Fu, magic), and_or(v4, 0x000F000Fu, magic),
-                             and_or(d[i] >> 8, 0x000F000Fu, magic), and_or(v4 >> 8, 0x000F000Fu, magic)};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {          // p[j] holds fields j and j + 4 of this dword
-        f[8 * i + j] = __builtin_fmaf(f16_lo(p[j]), s, so);
-        f[8 * i + j + 4] = __builtin_fmaf(f16_hi(p[j]), s, so);
-      }
-    }
-  } else if constexpr (Q == 2) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {          // fields j and j + 8 of this dword
-        const uint32_t p = and_or(d[i] >> (2 * j), 0x00030003u, magic);
-        f[16 * i + j] = __builtin_fmaf(f16_lo(p), s, so);
-        f[16 * i + j + 8] = __builtin_fmaf(f16_hi(p), s, so);
-      }
-  } else {
-    // Four 24-bit words of 8 fields; fields 4..7 of each word moved up to bit 16.
-    const uint32_t v[4] = {d[0], __builtin_amdgcn_alignbit(d[1], d[0], 24),
-                           __builtin_amdgcn_alignbit(d[2], d[1], 16), d[2] >> 8};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t sp = (v[i] & 0xFFFu) | ((v[i] << 4) & 0x0FFF0000u);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t p = and_or(sp >> (3 * j), 0x00070007u, magic);
-        f[8 * i + j] = __builtin_fmaf(f16_lo(p), s, so);
-        f[8 * i + j + 4] = __builtin_fmaf(f16_hi(p), s, so);
-      }
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < 16; ++k) w[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
-}
 
 // Tile order: workgroups are dealt round-robin to the 8 XCDs.  When the tile count
 // divides evenly, XCD x takes a contiguous run of tiles enumerated weight-panel
@@ -101,61 +57,50 @@ __device__ __forceinline__ void tile_of(int t, int tiles_m, int tiles_n, int& tm
   tm = t % tiles_m;
 }
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
 // ---------------------------------------------------------------------------
-// Split reduction (host side).  When the output has too few tiles to occupy the CUs
-// twice over, the K steps of each tile are divided among `splits` workgroups whose fp32
-// partial tiles meet in a caller-provided workspace: [counters: one u32 per tile,
-// padded to 256 bytes][partials: tiles x splits x BM x BN fp32].
+// Split reduction (host side).  When the output has too few tiles to give every CU
+// a workgroup, the K steps of each tile are divided among `splits` workgroups whose
+// fp32 partial tiles meet in a caller-provided workspace: [counters: one u32 per
+// tile, padded to 256 bytes][partials: tiles x splits x BM x BN fp32].
 // ---------------------------------------------------------------------------
-constexpr int64_t kTargetWorkgroups = 512;   // two resident workgroups per CU
 constexpr int kMinStepsPerSplit = 16;
+
 
 int64_t counter_bytes(int64_t tiles) { return (tiles * 4 + 255) / 256 * 256; }
 
-int desired_splits(int64_t M, int64_t N, int64_t K) {
-  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+struct Plan {
+  int wm;            // wave rows (tile height 64*wm)
+  int64_t tiles;
+  int splits;
+  int64_t workspace; // bytes needed when splits > 1
+};
+
+Plan plan_for(int64_t M, int64_t N, int64_t K) {
+  Plan p{};
+  p.wm = M > 128 ? 4 : 2;                                 // 256-row tiles unless M is small
+  const int64_t bm = 64 * p.wm;
+  p.tiles = ((M + bm - 1) / bm) * ((N + BN - 1) / BN);
   const int64_t steps = (K / 32 + 1) / 2;
-  int64_t s = kTargetWorkgroups / tiles;
+  // enough workgroups to fill every CU (one per CU at wm=4, two at wm=2)
+  int64_t s = (p.wm == 4 ? 256 : 512) / p.tiles;
   s = std::min<int64_t>(s, steps / kMinStepsPerSplit);
   s = std::min<int64_t>(s, 8);
-  return (int)std::max<int64_t>(s, 1);
+  p.splits = (int)std::max<int64_t>(s, 1);
+  p.workspace = p.splits > 1 ? counter_bytes(p.tiles) + p.tiles * p.splits * bm * BN * 4 : 0;
+  return p;
 }
 
-int64_t workspace_for(int64_t M, int64_t N, int64_t K, int splits) {
-  if (splits <= 1) return 0;
-  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  return counter_bytes(tiles) + tiles * splits * BM * BN * 4;
-}
-
-int gemm_splits(int64_t M, int64_t N, int64_t K, const void* workspace, size_t bytes) {
-  const int s = desired_splits(M, N, K);
-  if (s <= 1 || workspace == nullptr || (int64_t)bytes < workspace_for(M, N, K, s)) return 1;
-  return s;
-}
-
-// s_waitcnt on the vector-memory counter only (gfx9 encoding: vmcnt in bits 3:0 and
-// 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).  Loads complete in order,
-// so vmcnt <= N means everything but the last N loads has landed -- including loads
-// that write LDS directly, which the compiler does not track.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | 0x70 | 0xF00 | ((N >> 4) << 14));
-}
-
-template <int Q, int G, bool ZP>
-__global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ x, int M,
-                                                   const uint8_t* __restrict__ codes,
-                                                   const uint16_t* __restrict__ scales,
-                                                   const uint8_t* __restrict__ zp, int N, int K,
-                                                   uint16_t* __restrict__ y, int splits,
-                                                   float* __restrict__ partials,
-                                                   unsigned int* __restrict__ counters) {
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[(kAStages + kBStages) * kTileBytes];
+template <int Q, int G, bool ZP, int WM>
+__global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
+    const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
+    const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zp, int N, int K,
+    uint16_t* __restrict__ y, int splits, float* __restrict__ partials,
+    unsigned int* __restrict__ counters) {
+  using C = Cfg<WM>;
+  constexpr int BM = C::BM, P = C::kParts, D = C::kAhead;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[C::kLds];
   uint8_t* const As = smem;
-  uint8_t* const Bs = smem + kAStages * kTileBytes;
+  uint8_t* const Bs = smem + C::kAStages * C::kATileBytes;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -185,40 +130,41 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + n0 * groups_per_row, rows_b * groups_per_row * 2);
   const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + n0 * groups_per_row : zp, ZP ? rows_b * groups_per_row : 0);
 
-  // Activation tile: 16 wavefront loads of 1 KB straight into LDS.  Wave w issues loads
-  // 4w..4w+3; load j fills tile rows 8j..8j+7, lane i writing 16 bytes at 16*i, which
-  // is row 8j + i/8, swizzled chunk i%8 -- so lane i fetches logical chunk (i%8)^(row%8).
+  // Activation tile: BM/8 wavefront loads of 1 KB straight into LDS, four per wave.
+  // Load j fills tile rows 8j..8j+7, lane i writing 16 bytes at 16*i, which is row
+  // 8j + i/8, swizzled chunk i%8 -- so lane i fetches logical chunk (i%8)^(row%8).
   uint32_t a_off[4];
+  int a_chunk[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = 8 * (4 * wave + j) + (lane >> 3);
-    const int c = (lane & 7) ^ (r & 7);
-    a_off[j] = (uint32_t)r * K * 2 + c * 16;
+    a_chunk[j] = (lane & 7) ^ (r & 7);
+    a_off[j] = (uint32_t)r * K * 2 + a_chunk[j] * 16;
   }
   auto issue_a = [&](int lstep, int stage) {
     const int step = s_begin + lstep;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int c = (lane & 7) ^ ((8 * (4 * wave + j) + (lane >> 3)) & 7);
       // chunks past K (odd block count, last step) read out of range -> zeros
-      const uint32_t off = step * 64 + c * 8 < K ? a_off[j] + (uint32_t)step * 128 : 0x80000000u;
+      const uint32_t off = step * 64 + a_chunk[j] * 8 < K ? a_off[j] + (uint32_t)step * 128 : 0x80000000u;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          ra, (lds_ptr_t)(As + stage * kTileBytes + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
+          ra, (lds_ptr_t)(As + stage * C::kATileBytes + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
     }
   };
 
-  // Weight tile: thread t dequantizes 32-weight block (t % 2) of row t / 2.
-  const int lr = tid >> 1, lh = tid & 1;
+  // Weight tile: P threads share each 32-weight block; block (t/P) % 2 of row t/(2P).
+  const int bid = tid / P, part = tid % P;
+  const int lr = bid >> 1, lh = bid & 1;
   const uint32_t c_off = (uint32_t)lr * row_bytes + lh * (4 * Q);
-  uint32_t c_reg[2][Q], s_reg[2], z_reg[2];
+  uint32_t c_reg[D][Part<Q, P>::kDwords], s_reg[D], z_reg[D];
   auto issue_b = [&](int lstep, int slot) {
     const int step = s_begin + lstep;
     const int blk = 2 * step + lh;
     const bool in = blk < nblk;
-    uint32_t d[Q];
-    buffer_block_codes<Q>(rc, in ? c_off + (uint32_t)step * (8 * Q) : 0x80000000u, 0, d);
+    uint32_t d[Part<Q, P>::kDwords];
+    load_part<Q, P>(rc, in ? c_off + (uint32_t)step * (8 * Q) : 0x80000000u, part, d);
 #pragma unroll
-    for (int i = 0; i < Q; ++i) c_reg[slot][i] = d[i];
+    for (int i = 0; i < Part<Q, P>::kDwords; ++i) c_reg[slot][i] = d[i];
     const uint32_t gi = (uint32_t)lr * groups_per_row + (uint32_t)(blk / (G / 32));
     s_reg[slot] = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? gi * 2 : 0x80000000u, 0, 0);
     if constexpr (ZP) z_reg[slot] = __builtin_amdgcn_raw_buffer_load_b8(rz, in ? gi : 0x80000000u, 0, 0);
@@ -226,12 +172,13 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
   auto store_b = [&](int slot, int stage) {
     const float s = f16_bits_to_f32(s_reg[slot]);
     const float o = ZP ? (float)z_reg[slot] : kSymOffset;
-    uint32_t w[16];
-    dequant_block<Q>(c_reg[slot], s, -(1024.0f + o) * s, w);   // exact: 11-bit times 11-bit
-    uint8_t* dst = Bs + stage * kTileBytes;
+    uint32_t w[16 / P];
+    dequant_part<Q, P>(c_reg[slot], part, s, -(1024.0f + o) * s, w);   // exact: 11-bit x 11-bit
+    uint8_t* dst = Bs + stage * kBTileBytes;
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      *reinterpret_cast<uint4*>(dst + swz(lr, lh * 4 + e)) = uint4{w[4 * e], w[4 * e + 1], w[4 * e + 2], w[4 * e + 3]};
+    for (int e = 0; e < 4 / P; ++e)
+      *reinterpret_cast<uint4*>(dst + swz(lr, lh * 4 + (4 / P) * part + e)) =
+          uint4{w[4 * e], w[4 * e + 1], w[4 * e + 2], w[4 * e + 3]};
   };
 
   f32x4 acc[4][4];
@@ -241,8 +188,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
   auto mfma_step = [&](int step) {
-    const uint8_t* at = As + (step % kAStages) * kTileBytes;
-    const uint8_t* bt = Bs + (step % kBStages) * kTileBytes;
+    const uint8_t* at = As + (step % C::kAStages) * C::kATileBytes;
+    const uint8_t* bt = Bs + (step % kBStages) * kBTileBytes;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 a[4], b[4];
@@ -260,36 +207,55 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     }
   };
 
-  // Step s: issue loads for s+2, multiply stage s, dequantize codes of s+1, then wait
-  // for this wave's activation loads of s+1 and barrier.  Slots are static (the loop is
-  // unrolled by two) so the code registers never need dynamic indexing.
+  // Step s: issue loads for step s+D into code slot s%D, multiply stage s, dequantize
+  // the codes of step s+1 (slot (s+1)%D), wait until this wave's activation loads of
+  // step s+1 have landed, barrier.  The loop is unrolled by D so slots are static.
   auto step_body = [&](int s, auto slot_c) {
-    constexpr int kSlot = decltype(slot_c)::value;
-    const bool ahead = s + 2 < nsteps;
-    if (ahead) {
-      issue_a(s + 2, (s + 2) % kAStages);
-      issue_b(s + 2, kSlot);
+    constexpr int kLoad = decltype(slot_c)::value;
+    constexpr int kDeq = (kLoad + 1) % D;
+    if (s + D < nsteps) {
+      issue_a(s + D, (s + D) % C::kAStages);
+      issue_b(s + D, kLoad);
     }
     mfma_step(s);
-    if (s + 1 < nsteps) store_b(1 - kSlot, (s + 1) % kBStages);
-    if (ahead) wait_vmcnt<kLoadsPerStep>();
-    else wait_vmcnt<0>();
+    if (s + 1 < nsteps) store_b(kDeq, (s + 1) % kBStages);
+    // loads of steps s+2 .. s+D may stay in flight
+    const int pending = std::min(nsteps - 1, s + D) - (s + 1);
+    if constexpr (D == 2) {
+      if (pending >= 1) wait_vmcnt<kLoadsPerStep>(); else wait_vmcnt<0>();
+    } else {
+      if (pending >= 2) wait_vmcnt<2 * kLoadsPerStep>();
+      else if (pending == 1) wait_vmcnt<kLoadsPerStep>();
+      else wait_vmcnt<0>();
+    }
     __syncthreads();
   };
 
-  issue_a(0, 0);
-  issue_b(0, 0);
-  if (nsteps > 1) {
-    issue_a(1, 1);
-    issue_b(1, 1);
+#pragma unroll
+  for (int l = 0; l < D; ++l) {
+    if (l < nsteps) {
+      issue_a(l, l);
+      issue_b(l, l);
+    }
   }
   store_b(0, 0);
-  if (nsteps > 1) wait_vmcnt<kLoadsPerStep>();
-  else wait_vmcnt<0>();
+  {
+    const int pending = std::min(nsteps - 1, D - 1);   // steps 1..D-1 may stay in flight
+    if constexpr (D == 2) {
+      if (pending >= 1) wait_vmcnt<kLoadsPerStep>(); else wait_vmcnt<0>();
+    } else {
+      if (pending >= 2) wait_vmcnt<2 * kLoadsPerStep>();
+      else if (pending == 1) wait_vmcnt<kLoadsPerStep>();
+      else wait_vmcnt<0>();
+    }
+  }
   __syncthreads();
-  for (int s = 0; s < nsteps; s += 2) {
+  for (int s = 0; s < nsteps; s += D) {
     step_body(s, std::integral_constant<int, 0>{});
-    if (s + 1 < nsteps) step_body(s + 1, std::integral_constant<int, 1>{});
+    if (s + 1 < nsteps) step_body(s + 1, std::integral_constant<int, 1 % D>{});
+    if constexpr (D == 3) {
+      if (s + 2 < nsteps) step_body(s + 2, std::integral_constant<int, 2>{});
+    }
   }
 
   if (splits > 1) {
@@ -297,23 +263,33 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     // accumulators (coalesced), then count arrivals; the last arriving workgroup sums
     // all slices in a fixed order, writes y and resets the counter so the workspace
     // stays reusable.
+    //
+    // Coherence across XCDs: the partials are written and read only with device-scope
+    // atomic stores and loads (sc1), which write through to memory and read from it
+    // rather than from this XCD's L2.  A store's vmcnt is released only once memory has
+    // acknowledged it, so after the wait below every partial of this slice is visible
+    // device-wide before the arrival count (a device-coherent RMW) is bumped, and the
+    // last workgroup's loads, issued after it has read the count, see them.  A general
+    // device-scope fence would instead write back the whole L2 of the XCD in every
+    // workgroup (tens of microseconds once many fp32 partials are dirty in it).
     float* mine = partials + ((int64_t)tile_id * splits + split) * (BM * BN) + wave * 4096 + lane;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mine[((i * 4 + j) * 4 + r) * 64] = acc[i][j][r];
-    __threadfence();                       // release the partial to the whole device
+        for (int r = 0; r < 4; ++r)
+          __hip_atomic_store(mine + ((i * 4 + j) * 4 + r) * 64, acc[i][j][r], __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    wait_vmcnt<0>();                       // every partial store acknowledged by memory
     // The tile buffers are idle after the main loop; their first word carries the arrival
-    // count to the whole workgroup (a separate shared variable would push LDS past 80 KB
-    // and halve the workgroups per CU).
+    // count to the whole workgroup (a separate shared variable would push LDS past the
+    // per-CU budget the ring sizes are chosen for).
     unsigned int* arrived = reinterpret_cast<unsigned int*>(smem);
     __syncthreads();
     if (tid == 0) *arrived = atomicAdd(&counters[tile_id], 1u);
     __syncthreads();
     if (*arrived != (unsigned int)(splits - 1)) return;   // uniform across the workgroup
-    __threadfence();                       // acquire the other slices' partials
     // Sum every slice (this one included) in slice order, so the result does not depend
     // on which workgroup arrived last.
 #pragma unroll
@@ -321,16 +297,19 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
     for (int o = 0; o < splits; ++o) {
-      const float* part = partials + ((int64_t)tile_id * splits + o) * (BM * BN) + wave * 4096 + lane;
+      const float* part_o = partials + ((int64_t)tile_id * splits + o) * (BM * BN) + wave * 4096 + lane;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[i][j][r] += __builtin_nontemporal_load(part + ((i * 4 + j) * 4 + r) * 64);
+          for (int r = 0; r < 4; ++r)
+            acc[i][j][r] += __hip_atomic_load(part_o + ((i * 4 + j) * 4 + r) * 64, __ATOMIC_RELAXED,
+                                              __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (tid == 0) counters[tile_id] = 0u;
+    if (tid == 0) __hip_atomic_store(&counters[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -347,13 +326,19 @@ template <int Q, int G, bool ZP>
 hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                          const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, void* workspace,
                          size_t workspace_bytes, hipStream_t stream) {
-  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  const int splits = gemm_splits(M, N, K, workspace, workspace_bytes);
+  const Plan p = plan_for(M, N, K);
+  const bool split = p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace;
+  const int splits = split ? p.splits : 1;
   unsigned int* counters = static_cast<unsigned int*>(workspace);
-  float* partials = splits > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + counter_bytes(tiles))
-                               : nullptr;
-  gemm_kernel<Q, G, ZP><<<dim3((unsigned)(tiles * splits)), 256, 0, stream>>>(
-      x, (int)M, codes, scales, zp, (int)N, (int)K, y, splits, partials, counters);
+  float* partials = split ? reinterpret_cast<float*>(static_cast<char*>(workspace) + counter_bytes(p.tiles))
+                          : nullptr;
+  const dim3 grid((unsigned)(p.tiles * splits));
+  if (p.wm == 4)
+    gemm_kernel<Q, G, ZP, 4><<<grid, Cfg<4>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
+                                                                   (int)K, y, splits, partials, counters);
+  else
+    gemm_kernel<Q, G, ZP, 2><<<grid, Cfg<2>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
+                                                                   (int)K, y, splits, partials, counters);
   return hipGetLastError();
 }
 
@@ -367,8 +352,6 @@ hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
                    workspace, workspace_bytes, stream);
 }
 
-size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-  return (size_t)workspace_for(M, N, K, desired_splits(M, N, K));
-}
+size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return (size_t)plan_for(M, N, K).workspace; }
 
 }  // namespace ssq

@@ -1,0 +1,194 @@
+// Skinny-M matmul (batched decode, 2 <= M <= 32): y[M,N] = x[M,K] * What[N,K]^T.
+//
+// App. B.3 of the paper: What[n,k] = s[n,b] (u[n,k] - o[n,b]).  With a handful of
+// tokens the product is bound by streaming the packed weights, as the GEMV is, but a
+// per-token dot product would repeat the unpacking M times.  Here every weight is
+// dequantized once (s*(u - o), exact in fp32, rounded to bf16) straight into the B
+// operand of v_mfma_f32_16x16x32_bf16, and the tokens share it through the matrix
+// cores: one MFMA per 16 tokens per 512 weights.  Nothing is staged in LDS except
+// the final cross-wavefront sums.
+//
+// A workgroup owns 16 consecutive weight rows and the whole reduction; its
+// wavefronts split K into contiguous ranges of 128-wide super-blocks.  For the MFMA,
+// lane l works on weight row l % 16 and on the super-block's 32-weight block l / 16,
+// and holds the 32 activations of token l % 16 at the same k.  The super-block's
+// four MFMAs take chunk t (8 k values) of each lane's block.  The MFMA reduces over
+// whatever k each lane supplies, so operands that agree on the assignment give the
+// exact product.
+//
+// Loads do not use that layout: lane L reads row (or token) L / 4, piece L % 4, so
+// four neighbouring lanes cover one contiguous 64-byte span and the texture unit
+// serves a quad per access (with one row per lane it serves one lane per cycle, which
+// halves throughput).  A ds_bpermute per dword then moves each value to its MFMA lane,
+// and for the activations a 4x4 transpose across the four 16-lane rows
+// (v_permlane32_swap / v_permlane16_swap) turns "chunk c of block j" into "chunk j of
+// block c".
+#include <algorithm>
+
+#include "mfma_dequant.h"
+#include "ssq_internal.h"
+
+namespace ssq {
+namespace {
+
+constexpr int kMaxWaves = 16;
+constexpr uint32_t kOutOfRange = 0x80000000u;   // past every buffer's size: loads return 0
+
+template <int Q, int G, bool ZP, int MB>
+__global__ __launch_bounds__(1024) void skinny_kernel(
+    const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
+    const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zp, int N, int K,
+    uint16_t* __restrict__ y) {
+  __shared__ float red[kMaxWaves][MB * 256];   // per wave: its partial D tiles, lane order
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  // wave-uniform (scalar) so the super-block loop and its range tests stay in SGPRs and
+  // out-of-range loads are chosen by a scalar select, not by branching around them
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int waves = (int)(blockDim.x >> 6);
+  const int64_t n0 = (int64_t)blockIdx.x * 16;
+  const int nblk = K / 32, nsb = (nblk + 3) / 4;
+  const int per = (nsb + waves - 1) / waves;
+  const int sb_begin = std::min(nsb, wave * per);
+  const int sb_end = std::min(nsb, sb_begin + per);
+  const uint32_t row_bytes = (uint32_t)K * Q / 8;
+  const uint32_t groups_per_row = (uint32_t)(K / G);
+  constexpr float kSymOffset = (float)(1 << (Q - 1));
+
+  // Descriptors over this workgroup's rows (rows past N read zeros) and over x (tokens
+  // past M read zeros; M*K*2 < 2^28 for M <= 32).
+  const uint32_t rows = (uint32_t)std::min<int64_t>(16, N - n0);
+  const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + n0 * row_bytes, rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + n0 * groups_per_row, rows * groups_per_row * 2);
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + n0 * groups_per_row : zp, ZP ? rows * groups_per_row : 0);
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)M * (uint32_t)K * 2);
+
+  struct Slot {
+    uint32_t d[Part<Q, 1>::kDwords];
+    uint32_t s, z;
+    u32x4 a[MB][4];
+  };
+  // Loads of super-block sb; a slot past this wave's range issues the same loads out of
+  // range (they return zeros and move no data), so every iteration waits on a fixed count.
+  // load layout: lane -> (row lrow, piece lpiece); MFMA layout: lane l takes the value
+  // loaded by lane 4*(l%16) + l/16 (byte address `perm` for ds_bpermute)
+  const int lrow = lane >> 2, lpiece = lane & 3;
+  const int perm = (4 * (lane & 15) + (lane >> 4)) * 4;
+  auto load = [&](int sb, bool valid, Slot& t) {
+    const int blk = 4 * sb + lpiece;
+    const bool in = valid & (blk < nblk);
+    load_part<Q, 1>(rc, in ? (uint32_t)lrow * row_bytes + (uint32_t)blk * (4 * Q) : kOutOfRange, 0, t.d);
+    const uint32_t gi = (uint32_t)lrow * groups_per_row + (uint32_t)(blk / (G / 32));
+    t.s = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? gi * 2 : kOutOfRange, 0, 0);
+    if constexpr (ZP) t.z = __builtin_amdgcn_raw_buffer_load_b8(rz, in ? gi : kOutOfRange, 0, 0);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const uint32_t m = (uint32_t)(mb * 16 + lrow);
+      // block j of the super-block, chunk lpiece of it: 16 tokens x 64 contiguous bytes
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const bool inj = valid & (4 * sb + j < nblk);
+        const uint32_t off = inj ? (m * (uint32_t)K + (uint32_t)(128 * sb + 32 * j + 8 * lpiece)) * 2 : kOutOfRange;
+        t.a[mb][j] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, kStream);
+      }
+    }
+    // keep the loads where they are issued: the scheduler would otherwise move them
+    // down next to their use, which removes the prefetch distance
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  f32x4 acc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  auto compute = [&](Slot& t) {
+    // to the MFMA layout: codes, scale and zero point of (row l%16, block l/16); token
+    // l%16's chunk l/16 of block j in register j
+#pragma unroll
+    for (int i = 0; i < Part<Q, 1>::kDwords; ++i) t.d[i] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.d[i]);
+    t.s = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.s);
+    if constexpr (ZP) t.z = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.z);
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) t.a[mb][j][e] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.a[mb][j][e]);
+    // 4x4 transpose across the four 16-lane rows: register j of row c holds chunk c of
+    // block j; afterwards register j of row c holds chunk j of block c.
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        auto p02 = __builtin_amdgcn_permlane32_swap(t.a[mb][0][e], t.a[mb][2][e], false, false);
+        auto p13 = __builtin_amdgcn_permlane32_swap(t.a[mb][1][e], t.a[mb][3][e], false, false);
+        auto p01 = __builtin_amdgcn_permlane16_swap(p02[0], p13[0], false, false);
+        auto p23 = __builtin_amdgcn_permlane16_swap(p02[1], p13[1], false, false);
+        t.a[mb][0][e] = p01[0]; t.a[mb][1][e] = p01[1];
+        t.a[mb][2][e] = p23[0]; t.a[mb][3][e] = p23[1];
+      }
+    const float s = f16_bits_to_f32(t.s);
+    const float o = ZP ? (float)t.z : kSymOffset;
+    uint32_t w[16];
+    dequant_part<Q, 1>(t.d, 0, s, -(1024.0f + o) * s, w);   // exact: 11-bit x 11-bit products
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bf16x8 b = __builtin_bit_cast(bf16x8, u32x4{w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]});
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, t.a[mb][j]), b, acc[mb], 0, 0, 0);
+    }
+  };
+
+  // Register slots used in turn: no copies (which would wait for the prefetch) and no
+  // early exit between a load and its use (the compiler would sink the load past it).
+  // A slot past the range holds zeros (scale 0), so computing it adds nothing.
+  Slot s0, s1;
+  load(sb_begin, sb_begin < sb_end, s0);
+  for (int sb = sb_begin; sb < sb_end; sb += 2) {
+    load(sb + 1, sb + 1 < sb_end, s1);
+    compute(s0);
+    load(sb + 2, sb + 2 < sb_end, s0);
+    compute(s1);
+  }
+
+  // Cross-wavefront reduction: lane l of a wave holds D[4*(l/16) + r][l % 16] of each
+  // 16-token block; sum the waves' tiles in wave order and write bf16.
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][mb * 256 + r * 64 + lane] = acc[mb][r];
+  __syncthreads();
+  for (int t = tid; t < MB * 256; t += (int)blockDim.x) {
+    float sum = 0.0f;
+    for (int w = 0; w < waves; ++w) sum += red[w][t];
+    const int mb = t >> 8, r = (t >> 6) & 3, l = t & 63;
+    const int m = mb * 16 + 4 * (l >> 4) + r;
+    const int64_t n = n0 + (l & 15);
+    if (m < M && n < N) y[(int64_t)m * N + n] = f32_to_bf16_bits(sum);
+  }
+}
+
+template <int Q, int G, bool ZP>
+hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                           const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+  const int64_t nsb = (K / 32 + 3) / 4;
+  const int waves = (int)std::min<int64_t>(kMaxWaves, nsb);
+  const dim3 grid((unsigned)((N + 15) / 16)), block((unsigned)(64 * waves));
+  if (M <= 16)
+    skinny_kernel<Q, G, ZP, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+  else
+    skinny_kernel<Q, G, ZP, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_skinny_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
+                              const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
+                              int group, int q, uint16_t* y, hipStream_t stream) {
+  if (M < 2 || M > kSkinnyMaxM) return hipErrorInvalidValue;
+  SSQ_DISPATCH_QGZ(skinny_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y, stream);
+}
+
+}  // namespace ssq

@@ -10,7 +10,7 @@ namespace {
 
 constexpr int64_t kMaxElems = int64_t(1) << 40;   // rows*cols or N*K
 constexpr int64_t kMaxDim = int64_t(1) << 30;     // any single dimension (kernels index in int)
-constexpr int64_t kMaxK = int64_t(1) << 23;       // matmul reduction length (32-bit tile offsets)
+constexpr int64_t kMaxK = int64_t(1) << 22;       // matmul reduction length (32-bit tile offsets)
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 bool valid_q(int q) { return q == 2 || q == 3 || q == 4; }
@@ -48,6 +48,18 @@ int check_matmul(const void* x, int64_t M, const uint8_t* codes, const uint16_t*
   return SSQ_OK;
 }
 
+// bf16 matmul kernel choice by token count: streaming GEMV (M = 1), skinny-M MFMA
+// kernel (batched decode), tiled MFMA GEMM with an optional split reduction (prefill).
+int dispatch_bf16(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                  const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                  void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
+  if (M <= ssq::kSkinnyMaxM)
+    return status_of(ssq::launch_skinny_bf16(x, M, codes, scales, zp, N, K, group, q, y, stream));
+  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace,
+                                         workspace_bytes, stream));
+}
+
 }  // namespace
 
 extern "C" {
@@ -71,12 +83,11 @@ int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_
                hipStream_t stream) {
   const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
   if (st != SSQ_OK || M == 0 || N == 0) return st;
-  if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
-  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, nullptr, 0, stream));
+  return dispatch_bf16(x, M, codes, scales, zp, N, K, group, q, y, nullptr, 0, stream);
 }
 
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q) {
-  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M < 2 || N == 0) return 0;
+  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M <= ssq::kSkinnyMaxM || N == 0) return 0;
   return ssq::gemm_workspace_bytes(M, N, K);
 }
 
@@ -86,9 +97,7 @@ int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint
   const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
   if (st != SSQ_OK || M == 0 || N == 0) return st;
   if (workspace != nullptr && !aligned(workspace, 256)) return SSQ_EALIGN;
-  if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
-  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace,
-                                         workspace_bytes, stream));
+  return dispatch_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace, workspace_bytes, stream);
 }
 
 int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,

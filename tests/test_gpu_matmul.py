@@ -1,5 +1,5 @@
-"""GPU parity: ssq_matmul (GEMV at M = 1, MFMA GEMM at M >= 2) and ssq_matmul_f32
-against the binary64 CPU oracle.
+"""GPU parity: ssq_matmul (GEMV at M = 1, skinny-M MFMA kernel at 2 <= M <= 32, tiled
+MFMA GEMM above) and ssq_matmul_f32 against the binary64 CPU oracle.
 
 Tolerances (relative L2 over the compared outputs): 2e-2 for bf16 output and
 1e-3 for the binary32 path.  The GEMV, which keeps the weights exact and only
@@ -97,7 +97,38 @@ def test_gemm_ragged_all_formats(q, group, mode):
     check_matmul(w, x, group, q, mode, tag=f"gemm 200x300x{K}")
 
 
-@pytest.mark.parametrize("M", [2, 3, 16, 129])
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("mode", MODES)
+def test_skinny_all_formats(q, group, mode):
+    # batched decode (2 <= M <= 32): N=45 leaves a partial 16-row workgroup; K is an odd
+    # number of 32-blocks at g=32 and g=64, so the last 128-wide super-block is partial
+    K = {32: 1056, 64: 1088, 128: 1152}[group]
+    w = rand_w(45, K, seed=3 * q + group + mode)
+    x = synth.activations(7, K, seed=q * group)
+    check_matmul(w, x, group, q, mode, tag=f"skinny 7x45x{K}")
+
+
+@pytest.mark.parametrize("M", [2, 15, 16, 17, 31, 32])
+def test_skinny_token_counts(M):
+    # one and two 16-token MFMA blocks, both partial and full; K=14336 spreads 112
+    # super-blocks over 16 wavefronts
+    w = rand_w(40, 14336, seed=M)
+    x = synth.activations(M, 14336, seed=M)
+    for mode in MODES:
+        check_matmul(w, x, 32, 4, mode, tag=f"skinny M={M}")
+
+
+@pytest.mark.parametrize("K", [32, 64, 128, 4096 + 96])
+def test_skinny_short_and_odd_reductions(K):
+    # fewer super-blocks than wavefronts, a lone partial super-block, a partial last one
+    w = rand_w(33, K, seed=K + 1)
+    x = synth.activations(16, K, seed=K + 1)
+    for mode in MODES:
+        check_matmul(w, x, 32, 3, mode, tag=f"skinny K={K}")
+
+
+@pytest.mark.parametrize("M", [2, 3, 16, 32, 33, 129])
 def test_gemm_small_token_counts(M):
     w = rand_w(64, 512, seed=M)
     x = synth.activations(M, 512, seed=M)
@@ -186,7 +217,7 @@ def test_empty_matmul_is_a_noop():
     assert y.shape == (3, 0)
 
 
-@pytest.mark.parametrize("M", [1, 64])
+@pytest.mark.parametrize("M", [1, 16, 64])
 def test_graph_replay_matches_eager(M):
     """ssq_matmul captured in a HIP graph: every replay, with eager work in between,
     equals the eager result bit for bit."""
