@@ -106,11 +106,12 @@ __device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&x
 // load and its kRows code and scale loads before any arithmetic and consumes them
 // in issue order, so many small wavefronts stream and compute concurrently.
 // Partial sums meet through a DPP wavefront reduction and LDS.
+//
+// Every row has its own buffer descriptor whose range is the row (or empty for rows
+// past N), and all offsets travel in the range-checked VGPR offset: rows past N read
+// zeros and contribute nothing.
 #ifndef SSQ_GEMV_ROWS
 #define SSQ_GEMV_ROWS 4          // rows per team
-#endif
-#ifndef SSQ_GEMV_BLOCKS_PER_THREAD
-#define SSQ_GEMV_BLOCKS_PER_THREAD 1
 #endif
 constexpr int kRows = SSQ_GEMV_ROWS;
 constexpr int kMaxWaves = 16;
@@ -135,22 +136,53 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
   const uint32_t groups_per_row = (uint32_t)(K / G);
   const uint32_t magic = kMagic;
+  const int64_t rows_here = N - row0 < kRows ? (N - row0 > 0 ? N - row0 : 0) : kRows;
+
+  __amdgpu_buffer_rsrc_t rc[kRows], rs[kRows], rz[kRows];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    const bool live = r < rows_here;
+    const int64_t row = live ? row0 + r : 0;
+    rc[r] = make_rsrc(codes + row * row_bytes, live ? row_bytes : 0u);
+    rs[r] = make_rsrc(scales + row * groups_per_row, live ? groups_per_row * 2 : 0u);
+    rz[r] = make_rsrc(ZP ? zp + row * groups_per_row : zp, ZP && live ? groups_per_row : 0u);
+  }
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
 
   float yacc[kRows];
 #pragma unroll
   for (int r = 0; r < kRows; ++r) yacc[r] = 0.0f;
 
-  if (row0 < N) {
-    // Descriptors cover exactly this team's rows: loads of rows past N return zeros
-    // (zero codes and zero scales contribute nothing).
-    const uint32_t rows_here = (uint32_t)(N - row0 < kRows ? N - row0 : kRows);
-    const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + row0 * row_bytes, rows_here * row_bytes);
-    const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + row0 * groups_per_row, rows_here * groups_per_row * 2);
-    const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + row0 * groups_per_row : zp, ZP ? rows_here * groups_per_row : 0);
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
+  auto consume = [&](const uint32_t (&X)[16], const Block<Q> (&cb)[kRows], const uint32_t (&sbits)[kRows],
+                     const uint32_t (&zbits)[kRows]) {
+    float xs = 0.0f;  // sum of the block's activations
+#pragma unroll
+    for (int i = 0; i < 16; ++i) xs = dot2(X[i], kOnes, xs);
+    uint32_t xp[16];
+    permute_x<Q>(X, xp);
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      const float acc = block_dot<Q>(cb[r], xp, magic);
+      const float sc = f16_bits_to_f32(sbits[r]);
+      const float off = ZP ? kMagicValue + (float)zbits[r] : kSymOffset;
+      yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
+    }
+  };
+  auto load_rows = [&](int j, Block<Q> (&cb)[kRows], uint32_t (&sbits)[kRows], uint32_t (&zbits)[kRows]) {
+    const uint32_t coff = (uint32_t)j * (4 * Q);
+    const uint32_t goff = (uint32_t)(j / kBlocksPerGroup);
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      buffer_block_codes<Q>(rc[r], coff, 0, cb[r].d);
+      sbits[r] = __builtin_amdgcn_raw_buffer_load_b16(rs[r], goff * 2, 0, 0);
+      zbits[r] = ZP ? __builtin_amdgcn_raw_buffer_load_b8(rz[r], goff, 0, 0) : 0u;
+    }
+  };
+
+  if (rows_here > 0) {
     for (int j = t; j < nblk; j += team_threads) {
       // Loads first, in consumption order: the activation block, then per row its codes,
-      // scale (and zero point).  Row offsets are scalar, lane offsets shared by all rows.
+      // scale (and zero point).
       uint32_t X[16];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -159,25 +191,8 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
       }
       Block<Q> cb[kRows];
       uint32_t sbits[kRows], zbits[kRows];
-      const uint32_t goff = (uint32_t)(j / kBlocksPerGroup);
-#pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        buffer_block_codes<Q>(rc, (uint32_t)j * (4 * Q), r * row_bytes, cb[r].d);
-        sbits[r] = __builtin_amdgcn_raw_buffer_load_b16(rs, goff * 2, r * groups_per_row * 2, 0);
-        zbits[r] = ZP ? __builtin_amdgcn_raw_buffer_load_b8(rz, goff, r * groups_per_row, 0) : 0u;
-      }
-      float xs = 0.0f;  // sum of the block's activations
-#pragma unroll
-      for (int i = 0; i < 16; ++i) xs = dot2(X[i], kOnes, xs);
-      uint32_t xp[16];
-      permute_x<Q>(X, xp);
-#pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        const float acc = block_dot<Q>(cb[r], xp, magic);
-        const float sc = f16_bits_to_f32(sbits[r]);
-        const float off = ZP ? kMagicValue + (float)zbits[r] : kSymOffset;
-        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
-      }
+      load_rows(j, cb, sbits, zbits);
+      consume(X, cb, sbits, zbits);
     }
   }
 #pragma unroll
@@ -246,8 +261,7 @@ template <int Q, int G, bool ZP>
 hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
                          const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
   const int64_t nblk = K / 32;
-  const int64_t per_thread = SSQ_GEMV_BLOCKS_PER_THREAD;
-  const int team = (int)std::min<int64_t>(1024, ((nblk + per_thread - 1) / per_thread + 63) / 64 * 64);
+  const int team = (int)std::min<int64_t>(1024, (nblk + 63) / 64 * 64);
   const int teams = team >= 256 ? 1 : 256 / team;
   const int64_t rows_per_block = (int64_t)teams * kRows;
   const dim3 grid((unsigned)((N + rows_per_block - 1) / rows_per_block));

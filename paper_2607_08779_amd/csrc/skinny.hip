@@ -169,9 +169,228 @@ __global__ __launch_bounds__(1024) void skinny_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Split variant (caller workspace).  The kernel above re-reads every activation once
+// per 16 weight rows (for M = 16 tokens at K = 14336: 117 MB from L2 against 29 MB of
+// codes), which bounds it.  Here a workgroup owns 128 weight rows and one slice of K;
+// each 16-token x 128-k activation chunk is loaded once into LDS and read by all eight
+// wavefronts, and the slices of a row block meet in the workspace.
+// ---------------------------------------------------------------------------
+constexpr int kSplitWaves = 8;                 // 16 weight rows each
+constexpr int kSplitRows = 16 * kSplitWaves;
+constexpr int kChunk = 8;                      // super-blocks whose loads are in flight at once
+constexpr int kSplitTargetWorkgroups = 512;    // two per CU
+constexpr int kSplitMaxSplits = 64;
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+int64_t split_counter_bytes(int64_t row_blocks) { return (row_blocks * 4 + 255) / 256 * 256; }
+
+struct SplitPlan {
+  int64_t row_blocks;
+  int splits;
+  int mb;
+  int64_t workspace;
+};
+
+// Enough workgroups to fill the chip and, where the split count allows, at most one
+// chunk of super-blocks per slice (its loads then all go out before any arithmetic).
+SplitPlan split_plan(int64_t M, int64_t N, int64_t K) {
+  SplitPlan p{};
+  p.row_blocks = (N + kSplitRows - 1) / kSplitRows;
+  p.mb = M > 16 ? 2 : 1;
+  const int64_t nsb = (K / 32 + 3) / 4;
+  int64_t s = std::max<int64_t>(kSplitTargetWorkgroups / std::max<int64_t>(p.row_blocks, 1),
+                                (nsb + kChunk - 1) / kChunk);
+  s = std::min<int64_t>(s, std::min<int64_t>(nsb, kSplitMaxSplits));
+  p.splits = (int)std::max<int64_t>(s, 1);
+  p.workspace = p.splits > 1
+                    ? split_counter_bytes(p.row_blocks) + p.row_blocks * p.splits * kSplitWaves * p.mb * 256 * 4
+                    : 0;
+  return p;
+}
+
+template <int Q, int G, bool ZP, int MB>
+__global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
+    const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
+    const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zp, int N, int K,
+    uint16_t* __restrict__ y, int splits, float* __restrict__ partials,
+    unsigned int* __restrict__ counters) {
+  constexpr int kStage = MB * 16 * 128 * 2;    // MB*16 tokens x 128 k, bf16
+  __shared__ __attribute__((aligned(1024))) uint8_t xs[kChunk * kStage];
+  __shared__ unsigned int arrived;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int row_blocks = (N + kSplitRows - 1) / kSplitRows;
+  const int rb = (int)blockIdx.x % row_blocks, split = (int)blockIdx.x / row_blocks;
+  const int64_t n0 = (int64_t)rb * kSplitRows + wave * 16;      // this wavefront's rows
+  const int nblk = K / 32, nsb = (nblk + 3) / 4;
+  const int per = (nsb + splits - 1) / splits;
+  const int sb_begin = std::min(nsb, split * per);
+  const int nsteps = std::min(nsb, sb_begin + per) - sb_begin;
+  const uint32_t row_bytes = (uint32_t)K * Q / 8;
+  const uint32_t groups_per_row = (uint32_t)(K / G);
+  constexpr float kSymOffset = (float)(1 << (Q - 1));
+
+  const uint32_t rows = (uint32_t)std::max<int64_t>(0, std::min<int64_t>(16, N - n0));
+  const int64_t nb = rows ? n0 : 0;
+  const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + nb * row_bytes, rows * row_bytes);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + nb * groups_per_row, rows * groups_per_row * 2);
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + nb * groups_per_row : zp, ZP ? rows * groups_per_row : 0);
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)M * (uint32_t)K * 2);
+
+  // Activation chunk of a super-block in LDS (one stage per super-block of the chunk):
+  // token block mb at mb*4 KB, token m at m*256, the 16-byte piece q (k = 128*sb + 8q)
+  // at position q ^ m, so that the 16 lanes that read one MFMA operand row group hit 16
+  // distinct bank groups.  Wavefront w fetches the stage of super-block w of the chunk,
+  // 1 KB per load (tokens 4j..4j+3 of block mb): lane L takes position L%16 of token
+  // 4j + L/16, i.e. piece (L%16) ^ m -- four neighbouring lanes read one aligned 64 bytes.
+  const int d_m = lane >> 4;                   // + 4j
+  auto issue_x = [&](int c0) {
+    const int st = c0 + wave;
+    const int sb = sb_begin + st;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = 4 * j + d_m;
+        const int q = (lane & 15) ^ m;
+        const bool in = (st < nsteps) & (4 * sb + (q >> 2) < nblk);
+        const uint32_t off = ((uint32_t)(mb * 16 + m) * (uint32_t)K + (uint32_t)sb * 128 + 8 * q) * 2;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rx, (lds_ptr_t)(xs + wave * kStage + mb * 4096 + j * 1024), 16, in ? off : kOutOfRange, 0, 0, 0);
+      }
+  };
+  constexpr int kXLoads = 4 * MB;
+
+  // Codes: lane L loads row L/4, block L%4 of the super-block (quad-contiguous), and
+  // ds_bpermute hands lane l the codes of row l%16, block l/16.
+  const int lrow = lane >> 2, lpiece = lane & 3;
+  const int perm = (4 * (lane & 15) + (lane >> 4)) * 4;
+  struct Slot {
+    uint32_t d[Part<Q, 1>::kDwords];
+    uint32_t s, z;
+  };
+  auto issue_w = [&](int st, Slot& t) {
+    const int blk = 4 * (sb_begin + st) + lpiece;
+    const bool in = (st < nsteps) & (blk < nblk);
+    load_part<Q, 1>(rc, in ? (uint32_t)lrow * row_bytes + (uint32_t)blk * (4 * Q) : kOutOfRange, 0, t.d);
+    const uint32_t gi = (uint32_t)lrow * groups_per_row + (uint32_t)(blk / (G / 32));
+    t.s = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? gi * 2 : kOutOfRange, 0, 0);
+    if constexpr (ZP) t.z = __builtin_amdgcn_raw_buffer_load_b8(rz, in ? gi : kOutOfRange, 0, 0);
+  };
+  constexpr int kWLoads = 2 + (ZP ? 1 : 0);     // vector loads of issue_w
+
+  f32x4 acc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  const int am = lane & 15, ac = lane >> 4;     // MFMA operand row and 32-k block
+  auto compute = [&](Slot& t, int stage) {
+#pragma unroll
+    for (int i = 0; i < Part<Q, 1>::kDwords; ++i) t.d[i] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.d[i]);
+    t.s = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.s);
+    if constexpr (ZP) t.z = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.z);
+    const float s = f16_bits_to_f32(t.s);
+    const float o = ZP ? (float)t.z : kSymOffset;
+    uint32_t w[16];
+    dequant_part<Q, 1>(t.d, 0, s, -(1024.0f + o) * s, w);   // exact: 11-bit x 11-bit products
+    const uint8_t* xb = xs + stage * kStage + am * 256;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bf16x8 b = __builtin_bit_cast(bf16x8, u32x4{w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]});
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(xb + mb * 4096 + (((4 * ac + j) ^ am) << 4));
+        acc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[mb], 0, 0, 0);
+      }
+    }
+  };
+
+  // Per chunk of up to kChunk super-blocks: every load of the chunk is issued first
+  // (activations into LDS, then the codes of each super-block into its own register
+  // slot; past the slice they are out of range and return zeros), the activations are
+  // waited for and published with one barrier, and the super-blocks are then computed
+  // in order as their codes land.  The barrier also keeps the compiler from moving the
+  // code loads down to their (conditional) uses.
+  for (int c0 = 0; c0 < nsteps; c0 += kChunk) {
+    Slot sl[kChunk];
+    issue_x(c0);
+#pragma unroll
+    for (int i = 0; i < kChunk; ++i) issue_w(c0 + i, sl[i]);
+    wait_vmcnt<kChunk * kWLoads>();            // this wave's activation loads have landed
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kChunk; ++i)
+      if (c0 + i < nsteps) compute(sl[i], i);
+    if (c0 + kChunk < nsteps) __syncthreads();   // the next chunk reuses the stages
+  }
+
+  if (splits > 1) {
+    // Same protocol as the split GEMM: write-through partials, arrival count, the last
+    // workgroup of the row block sums the slices in slice order and resets the count.
+    float* mine = partials + (((int64_t)rb * splits + split) * kSplitWaves + wave) * (MB * 256) + lane;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        __hip_atomic_store(mine + mb * 256 + r * 64, acc[mb][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (tid == 0) arrived = atomicAdd(&counters[rb], 1u);
+    __syncthreads();
+    if (arrived != (unsigned int)(splits - 1)) return;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    // Eight slices per round trip: all loads of a round are issued before any add (a
+    // slice index past the count reloads slice 0 and is added as zero).
+    constexpr int kBatch = 8;
+    const float* base = partials + ((int64_t)rb * splits * kSplitWaves + wave) * (MB * 256) + lane;
+    for (int o0 = 0; o0 < splits; o0 += kBatch) {
+      float v[kBatch][MB * 4];
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const int o = o0 + i < splits ? o0 + i : 0;
+        const float* part = base + (int64_t)o * kSplitWaves * (MB * 256);
+#pragma unroll
+        for (int e = 0; e < MB * 4; ++e)
+          v[i][e] = __hip_atomic_load(part + (e >> 2) * 256 + (e & 3) * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i)
+#pragma unroll
+        for (int e = 0; e < MB * 4; ++e) acc[e >> 2][e & 3] += o0 + i < splits ? v[i][e] : 0.0f;
+    }
+    if (tid == 0) __hip_atomic_store(&counters[rb], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = mb * 16 + 4 * (lane >> 4) + r;
+      const int64_t n = n0 + (lane & 15);
+      if (m < M && n < N) y[(int64_t)m * N + n] = f32_to_bf16_bits(acc[mb][r]);
+    }
+}
+
 template <int Q, int G, bool ZP>
 hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
-                           const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+                           const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  const SplitPlan p = split_plan(M, N, K);
+  if (p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace) {
+    unsigned int* counters = static_cast<unsigned int*>(workspace);
+    float* partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + split_counter_bytes(p.row_blocks));
+    const dim3 grid((unsigned)(p.row_blocks * p.splits)), block(64 * kSplitWaves);
+    if (p.mb == 1)
+      skinny_split_kernel<Q, G, ZP, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
+                                                                   y, p.splits, partials, counters);
+    else
+      skinny_split_kernel<Q, G, ZP, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
+                                                                   y, p.splits, partials, counters);
+    return hipGetLastError();
+  }
   const int64_t nsb = (K / 32 + 3) / 4;
   const int waves = (int)std::min<int64_t>(kMaxWaves, nsb);
   const dim3 grid((unsigned)((N + 15) / 16)), block((unsigned)(64 * waves));
@@ -186,9 +405,13 @@ hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, c
 
 hipError_t launch_skinny_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
                               const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
-                              int group, int q, uint16_t* y, hipStream_t stream) {
+                              int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
   if (M < 2 || M > kSkinnyMaxM) return hipErrorInvalidValue;
-  SSQ_DISPATCH_QGZ(skinny_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y, stream);
+  SSQ_DISPATCH_QGZ(skinny_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y, workspace,
+                   workspace_bytes, stream);
 }
+
+size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K) { return (size_t)split_plan(M, N, K).workspace; }
 
 }  // namespace ssq

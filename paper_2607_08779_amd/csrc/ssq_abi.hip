@@ -55,7 +55,8 @@ int dispatch_bf16(const uint16_t* x, int64_t M, const uint8_t* codes, const uint
                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
   if (M <= ssq::kSkinnyMaxM)
-    return status_of(ssq::launch_skinny_bf16(x, M, codes, scales, zp, N, K, group, q, y, stream));
+    return status_of(ssq::launch_skinny_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace,
+                                             workspace_bytes, stream));
   return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace,
                                          workspace_bytes, stream));
 }
@@ -87,8 +88,8 @@ int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_
 }
 
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q) {
-  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M <= ssq::kSkinnyMaxM || N == 0) return 0;
-  return ssq::gemm_workspace_bytes(M, N, K);
+  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M < 2 || N == 0) return 0;
+  return M <= ssq::kSkinnyMaxM ? ssq::skinny_workspace_bytes(M, N, K) : ssq::gemm_workspace_bytes(M, N, K);
 }
 
 int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,

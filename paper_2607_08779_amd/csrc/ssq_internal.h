@@ -175,11 +175,13 @@ hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
 // Workspace bytes that let the GEMM split its reduction (0 when splitting would not help).
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
-// Token counts 2..kSkinnyMaxM run the skinny-M kernel (weights dequantized once into
-// MFMA operands, no LDS tiles, no workspace).
+// Token counts 2..kSkinnyMaxM run the skinny-M kernels (weights dequantized once into
+// MFMA operands; with a workspace the reduction is split across workgroups).
 constexpr int64_t kSkinnyMaxM = 32;
 hipError_t launch_skinny_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
                               const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
-                              int group, int q, uint16_t* y, hipStream_t stream);
+                              int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 }  // namespace ssq

@@ -99,6 +99,9 @@ def test_workspace_size_rules():
     assert n == 256 + 64 * 4 * 256 * 128 * 4           # counters (64 x u32, padded) + partials
     assert lib.ssq_matmul_workspace_size(2048, 14336, 4096, 32, 4) == 0   # enough tiles
     assert lib.ssq_matmul_workspace_size(1, 4096, 14336, 32, 4) == 0      # GEMV never splits
+    # batched decode: 32 row blocks of 128 rows, 16 slices of K, one 16-token block
+    assert lib.ssq_matmul_workspace_size(16, 4096, 14336, 32, 4) == 256 + 32 * 16 * 8 * 256 * 4
+    assert lib.ssq_matmul_workspace_size(32, 4096, 14336, 32, 4) == 256 + 32 * 16 * 8 * 512 * 4
     assert lib.ssq_matmul_workspace_size(512, 4096, 48, 32, 4) == 0       # invalid K
     assert lib.ssq_matmul_workspace_size(512, 4096, 256, 32, 4) == 0      # too few steps
 

@@ -151,10 +151,30 @@ def test_gemm_split_reduction_eight_ways():
     check_matmul(w, x, 128, 4, O.SIGNED_SYM, tag="split 64x160x8192", workspace=True, repeat=2)
 
 
-def test_split_reduction_graph_replay():
-    """The split GEMM in a HIP graph: the arrival counters reset inside the kernel, so
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("mode", MODES)
+def test_skinny_split_reduction_ragged(q, mode):
+    # batched decode with a workspace: N=200 is two 128-row blocks (the second partial),
+    # K=3104 has 25 super-blocks (the last one partial) over 12 slices (the last three
+    # empty); three calls on one workspace
+    w = rand_w(200, 3104, seed=q + 10 * mode + 1)
+    x = synth.activations(7, 3104, seed=q + 1)
+    check_matmul(w, x, 32, q, mode, tag="skinny split 7x200x3104", workspace=True, repeat=3)
+
+
+@pytest.mark.parametrize("M", [2, 16, 17, 32])
+@pytest.mark.parametrize("group", [32, 128])
+def test_skinny_split_token_counts(M, group):
+    w = rand_w(300, 8192, seed=M + group)
+    x = synth.activations(M, 8192, seed=M + group)
+    for mode in MODES:
+        check_matmul(w, x, group, 4, mode, tag=f"skinny split M={M}", workspace=True, repeat=2)
+
+
+@pytest.mark.parametrize("M,N,K", [(96, 256, 8192), (16, 256, 8192)])
+def test_split_reduction_graph_replay(M, N, K):
+    """The split kernels in a HIP graph: the arrival counters reset inside the kernel, so
     every replay (with eager work between) reproduces the first result."""
-    M, N, K = 96, 256, 8192
     W = to_device(rand_w(N, K, seed=8), True)
     codes, scales, _ = ssq.ssq_quantize(W, 32, 4, O.SIGNED_SYM)
     x = to_device(synth.activations(M, K, seed=8), True)
@@ -290,12 +310,12 @@ def test_prefill_headline_split_full_size():
                  tag="prefill down_proj M=512 split", workspace=True, repeat=2)
 
 
-@pytest.mark.parametrize("M", [1, 16])
-def test_llama3_70b_matmul_full_size(M):
+@pytest.mark.parametrize("M,workspace", [(1, False), (16, False), (16, True)])
+def test_llama3_70b_matmul_full_size(M, workspace):
     wl = synth.llama3_70b_block()
     for name in ("k_proj", "down_proj"):
         spec = wl.layers[name]
         w = synth.weights(spec)
         x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
         check_matmul(w, x, 32, 2, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=24, seed=M),
-                     tag=f"70b {name} M={M}")
+                     tag=f"70b {name} M={M}", workspace=workspace, repeat=2 if workspace else 1)
