@@ -20,7 +20,7 @@ LIB = os.path.join(PKG, "libssq.so")
 
 ARCH = "gfx950"
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",
     "-ffp-contract=off",                      # every fma in the kernels is written out
     "-mllvm", "-amdgpu-mfma-vgpr-form=1",     # MFMA accumulators in VGPRs: no AGPR copies in loops
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

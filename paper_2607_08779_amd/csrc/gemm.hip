@@ -16,6 +16,7 @@
 // internal k order.  Lane l receives D[4 * (l / 16) + r][l % 16], r = 0..3.
 #include <algorithm>
 #include <type_traits>
+#include <utility>
 
 #include "ssq_internal.h"
 #include "mfma_dequant.h"
@@ -97,12 +98,26 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     uint16_t* __restrict__ y, int splits, float* __restrict__ partials,
     unsigned int* __restrict__ counters) {
   using C = Cfg<WM>;
-  constexpr int BM = C::BM, P = C::kParts, D = C::kAhead;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[C::kLds];
-  uint8_t* const As = smem;
-  uint8_t* const Bs = smem + C::kAStages * C::kATileBytes;
+  constexpr int BM = C::BM, P = C::kParts, S = C::kAStages, D = C::kAhead;
+  // Activation stages: one LDS object each, named with compile-time indices only.
+  __shared__ __attribute__((aligned(1024))) uint8_t A0[C::kATileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t A1[C::kATileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t A2[C::kATileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t Bs[kBStages * kBTileBytes];
+  auto a_tile = [&](auto stage) -> uint8_t* {
+    constexpr int i = decltype(stage)::value;
+    static_assert(i < S, "stage index");
+    if constexpr (i == 0) return A0;
+    else if constexpr (i == 1) return A1;
+    else if constexpr (i == 2) return A2;
+    else {
+      __shared__ __attribute__((aligned(1024))) uint8_t A3[C::kATileBytes];
+      return A3;
+    }
+  };
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar offsets
   const int wm = wave >> 1, wn = wave & 1;
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const int tiles = tiles_m * tiles_n;
@@ -141,26 +156,34 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     a_chunk[j] = (lane & 7) ^ (r & 7);
     a_off[j] = (uint32_t)r * K * 2 + a_chunk[j] * 16;
   }
-  auto issue_a = [&](int lstep, int stage) {
+  // Activations go through registers: loaded D steps ahead, written to their stage one
+  // step before use (every wait is then one the compiler places on a register it needs).
+  u32x4 a_reg[S][4];
+  auto issue_a = [&](int lstep, int slot) {
     const int step = s_begin + lstep;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      // chunks past K (odd block count, last step) read out of range -> zeros
-      const uint32_t off = step * 64 + a_chunk[j] * 8 < K ? a_off[j] + (uint32_t)step * 128 : 0x80000000u;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          ra, (lds_ptr_t)(As + stage * C::kATileBytes + (4 * wave + j) * 1024), 16, off, 0, 0, 0);
+      // chunks past this slice or past K (odd block count, last step) read zeros
+      const bool in = (lstep < nsteps) & (step * 64 + a_chunk[j] * 8 < K);
+      const uint32_t off = in ? a_off[j] + (uint32_t)step * 128 : 0x80000000u;
+      a_reg[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, kStream);
     }
+  };
+  auto store_a = [&](int slot, auto stage) {
+    uint8_t* const at = a_tile(stage);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) *reinterpret_cast<u32x4*>(at + (4 * wave + j) * 1024 + lane * 16) = a_reg[slot][j];
   };
 
   // Weight tile: P threads share each 32-weight block; block (t/P) % 2 of row t/(2P).
   const int bid = tid / P, part = tid % P;
   const int lr = bid >> 1, lh = bid & 1;
   const uint32_t c_off = (uint32_t)lr * row_bytes + lh * (4 * Q);
-  uint32_t c_reg[D][Part<Q, P>::kDwords], s_reg[D], z_reg[D];
+  uint32_t c_reg[S][Part<Q, P>::kDwords], s_reg[S], z_reg[S];
   auto issue_b = [&](int lstep, int slot) {
     const int step = s_begin + lstep;
     const int blk = 2 * step + lh;
-    const bool in = blk < nblk;
+    const bool in = (lstep < nsteps) & (blk < nblk);
     uint32_t d[Part<Q, P>::kDwords];
     load_part<Q, P>(rc, in ? c_off + (uint32_t)step * (8 * Q) : 0x80000000u, part, d);
 #pragma unroll
@@ -187,8 +210,8 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  auto mfma_step = [&](int step) {
-    const uint8_t* at = As + (step % C::kAStages) * C::kATileBytes;
+  auto mfma_step = [&](int step, auto stage) {
+    const uint8_t* at = a_tile(stage);
     const uint8_t* bt = Bs + (step % kBStages) * kBTileBytes;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
@@ -210,53 +233,42 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   // Step s: issue loads for step s+D into code slot s%D, multiply stage s, dequantize
   // the codes of step s+1 (slot (s+1)%D), wait until this wave's activation loads of
   // step s+1 have landed, barrier.  The loop is unrolled by D so slots are static.
-  auto step_body = [&](int s, auto slot_c) {
-    constexpr int kLoad = decltype(slot_c)::value;
-    constexpr int kDeq = (kLoad + 1) % D;
-    if (s + D < nsteps) {
-      issue_a(s + D, (s + D) % C::kAStages);
-      issue_b(s + D, kLoad);
-    }
-    mfma_step(s);
-    if (s + 1 < nsteps) store_b(kDeq, (s + 1) % kBStages);
-    // loads of steps s+2 .. s+D may stay in flight
-    const int pending = std::min(nsteps - 1, s + D) - (s + 1);
-    if constexpr (D == 2) {
-      if (pending >= 1) wait_vmcnt<kLoadsPerStep>(); else wait_vmcnt<0>();
-    } else {
-      if (pending >= 2) wait_vmcnt<2 * kLoadsPerStep>();
-      else if (pending == 1) wait_vmcnt<kLoadsPerStep>();
-      else wait_vmcnt<0>();
-    }
+  // Step s (position p = s % S in a group of S steps): issue the loads of step s+D into
+  // slot (p+D) % S, multiply stage p, dequantize the codes of step s+1 and write its
+  // activations (slot (p+1) % S) to its weight and activation stages, barrier.  Every
+  // step issues and stores unconditionally -- past the slice the loads are out of range
+  // and return zeros -- and the loop runs whole groups of S steps (static stages and
+  // slots) with no exit between a load and its use; the last nsteps % S steps follow.
+  // Stage (p+1) % S was last read S-1 steps ago, before an earlier barrier; the barrier
+  // publishes step s+1's tiles.
+  auto step_body = [&](int s, auto pos) {
+    constexpr int p = decltype(pos)::value;
+    constexpr int kLoad = (p + D) % S;
+    constexpr int kNext = (p + 1) % S;
+    issue_a(s + D, kLoad);
+    issue_b(s + D, kLoad);
+    __builtin_amdgcn_sched_barrier(0);       // the loads go out first
+    mfma_step(s, pos);
+    store_b(kNext, (s + 1) % kBStages);
+    store_a(kNext, std::integral_constant<int, kNext>{});
     __syncthreads();
   };
 
-#pragma unroll
-  for (int l = 0; l < D; ++l) {
-    if (l < nsteps) {
-      issue_a(l, l);
-      issue_b(l, l);
-    }
-  }
+  [&]<int... L>(std::integer_sequence<int, L...>) {
+    ((issue_a(L, L), issue_b(L, L)), ...);
+  }(std::make_integer_sequence<int, D>{});
   store_b(0, 0);
-  {
-    const int pending = std::min(nsteps - 1, D - 1);   // steps 1..D-1 may stay in flight
-    if constexpr (D == 2) {
-      if (pending >= 1) wait_vmcnt<kLoadsPerStep>(); else wait_vmcnt<0>();
-    } else {
-      if (pending >= 2) wait_vmcnt<2 * kLoadsPerStep>();
-      else if (pending == 1) wait_vmcnt<kLoadsPerStep>();
-      else wait_vmcnt<0>();
-    }
-  }
+  store_a(0, std::integral_constant<int, 0>{});
   __syncthreads();
-  for (int s = 0; s < nsteps; s += D) {
-    step_body(s, std::integral_constant<int, 0>{});
-    if (s + 1 < nsteps) step_body(s + 1, std::integral_constant<int, 1 % D>{});
-    if constexpr (D == 3) {
-      if (s + 2 < nsteps) step_body(s + 2, std::integral_constant<int, 2>{});
-    }
+  int s = 0;
+  for (; s + S <= nsteps; s += S) {
+    [&]<int... L>(std::integer_sequence<int, L...>) {
+      (step_body(s + L, std::integral_constant<int, L>{}), ...);
+    }(std::make_integer_sequence<int, S>{});
   }
+  [&]<int... L>(std::integer_sequence<int, L...>) {
+    ((s + L < nsteps ? step_body(s + L, std::integral_constant<int, L>{}) : void()), ...);
+  }(std::make_integer_sequence<int, S - 1>{});
 
   if (splits > 1) {
     // Split reduction: publish this slice's fp32 partial tile in the lane order of the
@@ -285,7 +297,7 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     // The tile buffers are idle after the main loop; their first word carries the arrival
     // count to the whole workgroup (a separate shared variable would push LDS past the
     // per-CU budget the ring sizes are chosen for).
-    unsigned int* arrived = reinterpret_cast<unsigned int*>(smem);
+    unsigned int* arrived = reinterpret_cast<unsigned int*>(Bs);
     __syncthreads();
     if (tid == 0) *arrived = atomicAdd(&counters[tile_id], 1u);
     __syncthreads();
