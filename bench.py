@@ -55,7 +55,8 @@ def kernel_source_sha(files) -> str:
 
 KERNEL_SOURCES = {
     "gemv": ["gemv.hip", "ssq_internal.h"],
-    "gemm": ["gemm.hip", "ssq_internal.h"],
+    "gemm": ["gemm.hip", "mfma_dequant.h", "ssq_internal.h"],
+    "batched": ["skinny.hip", "mfma_dequant.h", "ssq_internal.h"],
     "quantize": ["quantize.hip", "ssq_internal.h"],
 }
 
@@ -84,7 +85,8 @@ def parse_args():
     p.add_argument("--gemm-m", type=int, default=512)
     p.add_argument("--mode", choices=["signed_sym", "unsigned_sym", "asym"], default="signed_sym")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--phases", default="quantize,gemv,gemm",
+    p.add_argument("--batched-m", type=int, default=16, help="tokens of the batched-decode phase")
+    p.add_argument("--phases", default="quantize,gemv,batched,gemm",
                    help="comma list of phases to run (profiling runs isolate one kernel); "
                         "'copy' adds a plain 256 MiB device copy used to calibrate byte counters")
     return p.parse_args()
@@ -161,12 +163,13 @@ def main() -> int:
     w_bits = synth.weights(spec)                                   # bf16 bits, host
     x1_bits = synth.activations(1, K, seed=wl.x_seed)
     xm_bits = synth.activations(args.gemm_m, K, seed=wl.x_seed + args.gemm_m)
+    xb_bits = synth.activations(args.batched_m, K, seed=wl.x_seed + args.batched_m)
 
     def dev_bf16(a):
         return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
 
     W = dev_bf16(w_bits)
-    x1, xm = dev_bf16(x1_bits), dev_bf16(xm_bits)
+    x1, xm, xb = dev_bf16(x1_bits), dev_bf16(xm_bits), dev_bf16(xb_bits)
     zp_on = mode == ssq.ASYM
     layers = []
     for _ in range(args.layers):
@@ -174,8 +177,11 @@ def main() -> int:
     staging = ssq.ssq_quantize(W, g, q, mode)                      # quantize target each step
     y1 = torch.empty((1, N), dtype=torch.bfloat16, device=dev)
     ym = torch.empty((args.gemm_m, N), dtype=torch.bfloat16, device=dev)
-    # the prefill GEMM gets the split-reduction workspace it asks for (None: no split)
+    yb = torch.empty((args.batched_m, N), dtype=torch.bfloat16, device=dev)
+    # the prefill GEMM and the batched decode get the split-reduction workspaces they ask
+    # for (None: no split)
     gemm_ws = ssq.ssq_matmul_workspace(args.gemm_m, N, K, g, q, device=dev)
+    batched_ws = ssq.ssq_matmul_workspace(args.batched_m, N, K, g, q, device=dev)
     torch.cuda.synchronize()
 
     # The decode GEMVs and prefill GEMMs of one step are captured once in a HIP graph
@@ -187,13 +193,17 @@ def main() -> int:
             for r in range(args.layers):
                 c, s, z = layers[(i + r) % args.layers]
                 ssq.ssq_matmul(x1, c, s, z, N, K, g, q, out=y1)
+        if "batched" in phases:
+            for r in range(args.layers):
+                c, s, z = layers[(i + r) % args.layers]
+                ssq.ssq_matmul(xb, c, s, z, N, K, g, q, out=yb, workspace=batched_ws)
         if "gemm" in phases:
             for r in range(args.gemm_layers):
                 c, s, z = layers[(i * args.gemm_layers + r) % args.layers]
                 ssq.ssq_matmul(xm, c, s, z, N, K, g, q, out=ym, workspace=gemm_ws)
 
     graphs = {}
-    for part in ("gemv", "gemm"):
+    for part in ("gemv", "batched", "gemm"):
         if part not in phases:
             continue
         saved = set(phases)
@@ -226,15 +236,19 @@ def main() -> int:
             graphs["gemv"].replay()
         if ev:
             ev[2].record()
+        if "batched" in graphs:
+            graphs["batched"].replay()
+        if ev:
+            ev[3].record()
         if "gemm" in graphs:
             graphs["gemm"].replay()
         if ev:
-            ev[3].record()
+            ev[4].record()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -251,13 +265,15 @@ def main() -> int:
 
     t_q = sum(e[0].elapsed_time(e[1]) for e in events) / 1e3   # seconds
     t_v = sum(e[1].elapsed_time(e[2]) for e in events) / 1e3
-    t_m = sum(e[2].elapsed_time(e[3]) for e in events) / 1e3
-    t_step = sum(e[0].elapsed_time(e[3]) for e in events) / 1e3 / args.steps
+    t_b = sum(e[2].elapsed_time(e[3]) for e in events) / 1e3
+    t_m = sum(e[3].elapsed_time(e[4]) for e in events) / 1e3
+    t_step = sum(e[0].elapsed_time(e[4]) for e in events) / 1e3 / args.steps
 
     zp_bytes = N * K // g if zp_on else 0
     gemv_bytes = N * K * q // 8 + 2 * N * K // g + zp_bytes + 2 * K + 2 * N
     quant_bytes = 2 * N * K + N * K * q // 8 + 2 * N * K // g + zp_bytes
     gemm_flops = 2 * args.gemm_m * N * K
+    batched_bytes = N * K * q // 8 + 2 * N * K // g + zp_bytes + 2 * args.batched_m * (K + N)
     n_gemv = args.steps * args.layers
     n_gemm = args.steps * args.gemm_layers
 
@@ -271,6 +287,8 @@ def main() -> int:
                    "group": g, "mode": args.mode, "decode_M": 1, "decode_layers": args.layers,
                    "prefill_M": args.gemm_m, "prefill_layers": args.gemm_layers,
                    "prefill_workspace_bytes": 0 if gemm_ws is None else gemm_ws.numel(),
+                   "batched_M": args.batched_m,
+                   "batched_workspace_bytes": 0 if batched_ws is None else batched_ws.numel(),
                    "weights": f"bf16 Student-t(5)*0.02 + 0.1% x20 outliers, seed {spec.seed}"},
         "wall_s": round(wall, 4),
     }
@@ -283,6 +301,16 @@ def main() -> int:
                            "traffic": measured_traffic("gemv"),
                            "kernel": "gemv_kernel (ssq_matmul, M=1)",
                            "bytes_per_launch": gemv_bytes, "avg_launch_us": round(avg * 1e6, 3)}
+    if "batched" in phases:
+        avg = t_b / n_gemv
+        gbs = batched_bytes / avg / 1e9
+        out["batched_decode_gbs"] = round(gbs, 2)
+        out["roofline_batched"] = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
+                                   "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                                   "traffic": measured_traffic("batched"),
+                                   "kernel": f"skinny_split_kernel (ssq_matmul, M={args.batched_m})",
+                                   "bytes_per_launch": batched_bytes, "avg_launch_us": round(avg * 1e6, 3),
+                                   "tflops": round(2 * args.batched_m * N * K / avg / 1e12, 2)}
     if "gemm" in phases:
         avg = t_m / n_gemm
         tf = gemm_flops / avg / 1e12
