@@ -4,11 +4,11 @@
 // dense contraction, so it runs on bf16 MFMA.  A workgroup of 2*WM wavefronts owns
 // a (64*WM) x 128 output tile, each wavefront a 64x64 sub-tile of
 // v_mfma_f32_16x16x32_bf16 (fp32 accumulation).  Per 64-deep step the activation
-// tile streams from memory straight into an LDS ring (buffer_load ... lds, several
-// steps ahead), weight codes are prefetched into registers and dequantized one step
-// ahead (s*(u - o), exact in fp32, rounded to bf16) into a second LDS ring; one
-// barrier per step.  WM=4 uses the full 160 KB of LDS (one workgroup per CU, a
-// four-stage activation ring); WM=2 fits two workgroups per CU.
+// tile and the weight codes are loaded into registers several steps ahead; one step
+// ahead the activations are written to an LDS ring and the codes dequantized
+// (s*(u - o), exact in fp32, rounded to bf16) into a second one; one barrier per step.
+// WM=4 uses the full 160 KB of LDS (one workgroup per CU, a four-stage activation
+// ring); WM=2 fits two workgroups per CU.
 //
 // MFMA operand layout (16x16x32): lane l supplies row (l % 16) of A and column
 // (l % 16) of B, each with 8 consecutive k values starting at 8 * (l / 16).
@@ -24,7 +24,6 @@
 namespace ssq {
 namespace {
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int BN = 128, BK = 64;
 constexpr int kBTileBytes = BN * BK * 2;     // 16 KB: 128 rows of 128 bytes
@@ -43,9 +42,11 @@ struct Cfg {
 };
 
 // Byte offset of 16-byte chunk c (8 bf16 along k) of row r in a tile.  The chunk index
-// is XOR-swizzled with the row, so the 16 rows an MFMA operand read touches at one k
-// offset fall in 8 different chunk columns (no padding needed).
-__device__ __forceinline__ uint32_t swz(int r, int c) { return (uint32_t)(r * 128 + ((c ^ (r & 7)) << 4)); }
+// is XOR-swizzled with r/2: an MFMA operand read touches 16 consecutive rows at one k
+// offset, and LDS serves 16 lanes of a 16-byte read per cycle across 256 bytes of banks,
+// so two neighbouring 128-byte rows share a bank line; r/2 sends each pair to its own
+// eighth of it (no padding needed).
+__device__ __forceinline__ uint32_t swz(int r, int c) { return (uint32_t)(r * 128 + ((c ^ ((r >> 1) & 7)) << 4)); }
 
 // Tile order: workgroups are dealt round-robin to the 8 XCDs.  When the tile count
 // divides evenly, XCD x takes a contiguous run of tiles enumerated weight-panel
@@ -65,6 +66,7 @@ __device__ __forceinline__ void tile_of(int t, int tiles_m, int tiles_n, int& tm
 // tile, padded to 256 bytes][partials: tiles x splits x BM x BN fp32].
 // ---------------------------------------------------------------------------
 constexpr int kMinStepsPerSplit = 16;
+
 
 
 int64_t counter_bytes(int64_t tiles) { return (tiles * 4 + 255) / 256 * 256; }
@@ -147,13 +149,13 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
 
   // Activation tile: BM/8 wavefront loads of 1 KB straight into LDS, four per wave.
   // Load j fills tile rows 8j..8j+7, lane i writing 16 bytes at 16*i, which is row
-  // 8j + i/8, swizzled chunk i%8 -- so lane i fetches logical chunk (i%8)^(row%8).
+  // 8j + i/8, swizzled chunk i%8 -- so lane i fetches logical chunk (i%8)^((row/2)%8).
   uint32_t a_off[4];
   int a_chunk[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = 8 * (4 * wave + j) + (lane >> 3);
-    a_chunk[j] = (lane & 7) ^ (r & 7);
+    a_chunk[j] = (lane & 7) ^ ((r >> 1) & 7);
     a_off[j] = (uint32_t)r * K * 2 + a_chunk[j] * 16;
   }
   // Activations go through registers: loaded D steps ahead, written to their stage one
@@ -213,6 +215,8 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   auto mfma_step = [&](int step, auto stage) {
     const uint8_t* at = a_tile(stage);
     const uint8_t* bt = Bs + (step % kBStages) * kBTileBytes;
+    // LLVM's MFMA/DS-read interleaving strategy for this loop shape (measured ~7 % faster)
+    __builtin_amdgcn_iglp_opt(1);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       bf16x8 a[4], b[4];
@@ -230,9 +234,6 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     }
   };
 
-  // Step s: issue loads for step s+D into code slot s%D, multiply stage s, dequantize
-  // the codes of step s+1 (slot (s+1)%D), wait until this wave's activation loads of
-  // step s+1 have landed, barrier.  The loop is unrolled by D so slots are static.
   // Step s (position p = s % S in a group of S steps): issue the loads of step s+D into
   // slot (p+D) % S, multiply stage p, dequantize the codes of step s+1 and write its
   // activations (slot (p+1) % S) to its weight and activation stages, barrier.  Every

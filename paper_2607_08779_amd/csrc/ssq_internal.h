@@ -175,6 +175,7 @@ hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
 // Workspace bytes that let the GEMM split its reduction (0 when splitting would not help).
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
+
 // Token counts 2..kSkinnyMaxM run the skinny-M kernels (weights dequantized once into
 // MFMA operands; with a workspace the reduction is split across workgroups).
 constexpr int64_t kSkinnyMaxM = 32;

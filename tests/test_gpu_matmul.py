@@ -171,7 +171,7 @@ def test_skinny_split_token_counts(M, group):
         check_matmul(w, x, group, 4, mode, tag=f"skinny split M={M}", workspace=True, repeat=2)
 
 
-@pytest.mark.parametrize("M,N,K", [(96, 256, 8192), (16, 256, 8192)])
+@pytest.mark.parametrize("M,N,K", [(96, 256, 8192), (300, 256, 8192), (16, 256, 8192)])
 def test_split_reduction_graph_replay(M, N, K):
     """The split kernels in a HIP graph: the arrival counters reset inside the kernel, so
     every replay (with eager work between) reproduces the first result."""
