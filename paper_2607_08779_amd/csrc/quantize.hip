@@ -16,7 +16,7 @@ namespace ssq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;   // chunks per thread, loaded before any is processed
+constexpr int kUnroll = 2;   // chunks per thread, loaded before any is processed (1, 4, 8 measured slower)
 
 template <typename In>
 struct Loader;
@@ -43,15 +43,20 @@ struct Loader<float> {  // binary32, 32 bytes per chunk
 
 // Store the 8q bits `v` of chunk `chunk` (its bytes start at chunk*q) as whole dwords.
 // Every lane must call this (the neighbour exchange is a wavefront shuffle).
+// The value of the next lane (DPP row_shl:1; the partners below never cross a 16-lane row).
+__device__ __forceinline__ uint32_t next_lane(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x101, 0xF, 0xF, false);
+}
+
 template <int Q>
 __device__ __forceinline__ void store_codes(uint8_t* codes, int64_t chunk, uint32_t v, bool valid) {
   if constexpr (Q == 4) {
     if (valid) reinterpret_cast<uint32_t*>(codes)[chunk] = v;
   } else if constexpr (Q == 2) {
-    const uint32_t next = __shfl_down(v, 1, 64);
+    const uint32_t next = next_lane(v);
     if (valid && (chunk & 1) == 0) reinterpret_cast<uint32_t*>(codes)[chunk >> 1] = v | (next << 16);
   } else {  // Q == 3: the 24-bit words of four lanes form three dwords
-    const uint32_t next = __shfl_down(v, 1, 64);
+    const uint32_t next = next_lane(v);
     const int j = (int)(chunk & 3);
     if (valid && j < 3)
       reinterpret_cast<uint32_t*>(codes)[(chunk >> 2) * 3 + j] = (v >> (8 * j)) | (next << (24 - 8 * j));
@@ -113,13 +118,20 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
         // (one fma against 3072, whose ulp is 2^-12) lands exactly on the half when the
         // quotient is one and on the correct side otherwise, so rint of the snapped value
         // equals rint(fl32(w/s)) -- the division result -- bit for bit.
+        //
+        // The snapped value t = 3072 + q' (|q'| <= 2^(q-1), a multiple of 2^-12) plus
+        // 1.5*2^23 - 3072 is 1.5*2^23 + q' exactly, rounded once at ulp 1: the low mantissa
+        // bits then hold rne(q') = c, and bits - bits(1.5*2^23) + 2^(q-1) is the offset-binary
+        // index u in [0, 2^q].  |w| <= M keeps c >= -2^(q-1), so only the top clip can bind.
         float rs = (1.0f / amax) * kHalfRange;
         if (neg) rs = -rs;
+        constexpr float kRound = 12582912.0f - 3072.0f;                    // 1.5*2^23 - 3072
+        constexpr uint32_t kBias = 0x4B400000u - (1u << (Q - 1));          // bits(1.5*2^23) - 2^(q-1)
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const float t = __builtin_fmaf(w[u][i], rs, 3072.0f) - 3072.0f;
-          const float c = fminf(fmaxf(rintf(t), kLo), kHi);
-          packed |= (uint32_t)((int)c + (1 << (Q - 1))) << (Q * i);
+          const float t = __builtin_fmaf(w[u][i], rs, 3072.0f);
+          const uint32_t idx = __float_as_uint(t + kRound) - kBias;
+          packed |= min(idx, (uint32_t)kTop) << (Q * i);
         }
       } else {
 #pragma unroll

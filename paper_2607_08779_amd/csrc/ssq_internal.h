@@ -102,10 +102,22 @@ __device__ __forceinline__ float f16_bits_to_f32(uint32_t bits) {
 }
 
 // Butterfly reduction over aligned lane sets of `width` lanes (width a power of two <= 64).
+// Maximum over aligned groups of WIDTH (4, 8 or 16) lanes, in every lane of the group,
+// with DPP moves (no LDS round trip): quad_perm xor 1 and xor 2 make each quad uniform,
+// row_half_mirror pairs the two quads of an 8-lane half-row, row_mirror the two halves
+// of a 16-lane row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_max(float v) {
+  const int moved = __builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false);
+  return fmaxf(v, __int_as_float(moved));
+}
 template <int WIDTH>
 __device__ __forceinline__ float group_max(float v) {
-#pragma unroll
-  for (int o = 1; o < WIDTH; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  static_assert(WIDTH == 4 || WIDTH == 8 || WIDTH == 16, "group of 4, 8 or 16 lanes");
+  v = dpp_max<0xB1>(v);                          // quad_perm [1,0,3,2]
+  v = dpp_max<0x4E>(v);                          // quad_perm [2,3,0,1]
+  if constexpr (WIDTH >= 8) v = dpp_max<0x141>(v);   // row_half_mirror
+  if constexpr (WIDTH >= 16) v = dpp_max<0x140>(v);  // row_mirror
   return v;
 }
 
