@@ -99,54 +99,90 @@ __device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&x
   return acc;
 }
 
-// Work split.  A team of T threads (T = blocks per row rounded up to whole
-// wavefronts, at most 1024) owns kRows consecutive rows; thread t takes block t of
-// each row (and t + T, ... for rows longer than 1024 blocks).  Short rows pack
-// several teams into one 256-thread workgroup.  Each thread issues its activation
-// load and its kRows code and scale loads before any arithmetic and consumes them
-// in issue order, so many small wavefronts stream and compute concurrently.
-// Partial sums meet through a DPP wavefront reduction and LDS.
+// Work split.  A workgroup of T threads (T a whole number of wavefronts, at most 512)
+// owns kRows consecutive rows; wavefront w takes 64 consecutive blocks of each row per
+// pass (lane i block 64w + i), and passes repeat T blocks further on until the row
+// ends.  Partial sums meet through a DPP wavefront reduction and LDS.  Every wavefront
+// of the grid is resident at once for the decode shapes, so the whole matrix is in
+// flight from the start; per-wavefront set-up is kept to a few scalar instructions,
+// because the CU's one scalar unit serves all of its wavefronts as they start.
 //
-// Every row has its own buffer descriptor whose range is the row (or empty for rows
-// past N), and all offsets travel in the range-checked VGPR offset: rows past N read
-// zeros and contribute nothing.
+// Operand movement.  The codes are loaded one block per lane (4q contiguous bytes,
+// lanes contiguous).  A lane also needs its block's 64 bytes of activations and one
+// scale per row, but loading those per lane would stride the activation loads by 64
+// bytes and spend a load instruction per row on two-byte scales.  Instead the
+// wavefront loads its 4 KB activation span with four fully contiguous 1 KB loads and
+// its kRows rows of scales (and zero points) with a single load, writes them to a
+// wavefront-private LDS area and reads back what each lane needs.  The activation
+// chunks are stored swizzled so that both the stores and the 64-byte-strided reads
+// hit distinct LDS banks.  The single scale load needs the rows' scale runs 16-byte
+// aligned; otherwise (VS = false) every lane loads its scale per row directly.
+//
+// One buffer descriptor covers the workgroup's live rows of codes (scales, zero
+// points) and one the activations; loads past a descriptor's range return zeros.
+// Lanes past the end of a row point their loads out of range, so rows and blocks
+// beyond the matrix contribute exact zeros.
 #ifndef SSQ_GEMV_ROWS
-#define SSQ_GEMV_ROWS 4          // rows per team
+#define SSQ_GEMV_ROWS 4          // rows per workgroup
 #endif
 constexpr int kRows = SSQ_GEMV_ROWS;
-constexpr int kMaxWaves = 16;
+constexpr int kMaxTeam = 512;
+constexpr int kMaxWaves = kMaxTeam / 64;
+constexpr int kXChunks = 256;    // 16-byte activation chunks of one pass: 64 blocks x 64 bytes
+constexpr uint32_t kOutOfRange = 0x80000000u;
 
-template <int Q, int G, bool ZP>
-__global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__ x,
-                                                    const uint8_t* __restrict__ codes,
-                                                    const uint16_t* __restrict__ scales,
-                                                    const uint8_t* __restrict__ zp, int N, int K,
-                                                    int team_threads, uint16_t* __restrict__ y) {
-  constexpr int kBlocksPerGroup = G / 32;
+template <int G, bool ZP>
+struct Stage {
+  static constexpr int kBlocksPerGroup = G / 32;
+  static constexpr int kScaleBytes = 128 / kBlocksPerGroup;   // one row's scales for 64 blocks
+  static constexpr int kZpBytes = 64 / kBlocksPerGroup;
+  static constexpr int kScaleChunks = kRows * kScaleBytes / 16;
+  static constexpr int kZpChunks = ZP ? kRows * kZpBytes / 16 : 0;
+  static constexpr int kWaveChunks = kXChunks + kScaleChunks + kZpChunks;
+  static constexpr int kWaveBytes = kWaveChunks * 16;
+  static_assert(kScaleChunks <= 64 && kZpChunks <= 64, "one load instruction per wavefront");
+};
+
+// LDS chunk holding piece p (16 bytes) of block b of a pass.
+__device__ __forceinline__ int x_slot(int b, int p) { return 4 * b + (p ^ ((b >> 2) & 3)); }
+
+// Orders LDS stores of some lanes before loads of others within one wavefront.
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int Q, int G, bool ZP, bool VS>
+__global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restrict__ x,
+                                                        const uint8_t* __restrict__ codes,
+                                                        const uint16_t* __restrict__ scales,
+                                                        const uint8_t* __restrict__ zp, int N, int K,
+                                                        uint16_t* __restrict__ y) {
+  using S = Stage<G, ZP>;
+  constexpr int kBlocksPerGroup = S::kBlocksPerGroup;
   constexpr float kSymOffset = kMagicValue + (float)(1 << (Q - 1));
   __shared__ float partial[kMaxWaves][kRows];
+  extern __shared__ u32x4 stage[];
 
-  // team_threads is a multiple of 64, so the team index is uniform across a wavefront.
-  const int team = __builtin_amdgcn_readfirstlane((int)threadIdx.x / team_threads);
-  const int t = (int)threadIdx.x - team * team_threads;
-  const int teams = blockDim.x / team_threads;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t row0 = ((int64_t)blockIdx.x * teams + team) * kRows;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int threads = blockDim.x;
+  const int row0 = (int)blockIdx.x * kRows;
+  const int rows_here = N - row0 < kRows ? N - row0 : kRows;   // >= 1
   const int nblk = K / 32;
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
-  const uint32_t groups_per_row = (uint32_t)(K / G);
+  const uint32_t groups_per_row = (uint32_t)K / G;
   const uint32_t magic = kMagic;
-  const int64_t rows_here = N - row0 < kRows ? (N - row0 > 0 ? N - row0 : 0) : kRows;
+  u32x4* const xw = stage + wave * S::kWaveChunks;
+  const uint8_t* const sw = reinterpret_cast<const uint8_t*>(xw + kXChunks);
+  const uint8_t* const zw = sw + S::kScaleChunks * 16;
 
-  __amdgpu_buffer_rsrc_t rc[kRows], rs[kRows], rz[kRows];
-#pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-    const bool live = r < rows_here;
-    const int64_t row = live ? row0 + r : 0;
-    rc[r] = make_rsrc(codes + row * row_bytes, live ? row_bytes : 0u);
-    rs[r] = make_rsrc(scales + row * groups_per_row, live ? groups_per_row * 2 : 0u);
-    rz[r] = make_rsrc(ZP ? zp + row * groups_per_row : zp, ZP && live ? groups_per_row : 0u);
-  }
+  const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + (int64_t)row0 * row_bytes, (uint32_t)rows_here * row_bytes);
+  const __amdgpu_buffer_rsrc_t rs =
+      make_rsrc(scales + (int64_t)row0 * groups_per_row, (uint32_t)rows_here * groups_per_row * 2);
+  const __amdgpu_buffer_rsrc_t rz =
+      make_rsrc(ZP ? zp + (int64_t)row0 * groups_per_row : zp, ZP ? (uint32_t)rows_here * groups_per_row : 0u);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
 
   float yacc[kRows];
@@ -168,47 +204,89 @@ __global__ __launch_bounds__(1024) void gemv_kernel(const uint16_t* __restrict__
       yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
     }
   };
-  auto load_rows = [&](int j, Block<Q> (&cb)[kRows], uint32_t (&sbits)[kRows], uint32_t (&zbits)[kRows]) {
-    const uint32_t coff = (uint32_t)j * (4 * Q);
-    const uint32_t goff = (uint32_t)(j / kBlocksPerGroup);
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      buffer_block_codes<Q>(rc[r], coff, 0, cb[r].d);
-      sbits[r] = __builtin_amdgcn_raw_buffer_load_b16(rs[r], goff * 2, 0, 0);
-      zbits[r] = ZP ? __builtin_amdgcn_raw_buffer_load_b8(rz[r], goff, 0, 0) : 0u;
-    }
-  };
 
-  if (rows_here > 0) {
-    for (int j = t; j < nblk; j += team_threads) {
-      // Loads first, in consumption order: the activation block, then per row its codes,
-      // scale (and zero point).
-      uint32_t X[16];
+  // Passes are uniform across the wavefront.
+  for (int jw = wave * 64; jw < nblk; jw += threads) {
+    const int j = jw + lane;
+    const bool live = j < nblk;
+    // Loads first: activations, scales (and zero points), then the codes of each row.
+    u32x4 xq[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rx, j * 64 + 16 * i, 0, 0);
-        X[4 * i] = v.x; X[4 * i + 1] = v.y; X[4 * i + 2] = v.z; X[4 * i + 3] = v.w;
+    for (int i = 0; i < 4; ++i) xq[i] = __builtin_amdgcn_raw_buffer_load_b128(rx, jw * 64 + 1024 * i + 16 * lane, 0, 0);
+    u32x4 sq = {0, 0, 0, 0}, zq = {0, 0, 0, 0};
+    uint32_t sbits[kRows], zbits[kRows];
+    if constexpr (VS) {
+      constexpr int kPer = S::kScaleBytes / 16;   // chunks per row
+      const uint32_t in_row = (uint32_t)(jw / kBlocksPerGroup) * 2 + 16 * (lane % kPer);
+      const uint32_t off = in_row < groups_per_row * 2 ? (lane / kPer) * groups_per_row * 2 + in_row : kOutOfRange;
+      if (lane < S::kScaleChunks) sq = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+      if constexpr (ZP) {
+        constexpr int kZPer = S::kZpBytes / 16;
+        const uint32_t zin = (uint32_t)(jw / kBlocksPerGroup) + 16 * (lane % kZPer);
+        const uint32_t zoff = zin < groups_per_row ? (lane / kZPer) * groups_per_row + zin : kOutOfRange;
+        if (lane < S::kZpChunks) zq = __builtin_amdgcn_raw_buffer_load_b128(rz, zoff, 0, 0);
       }
-      Block<Q> cb[kRows];
-      uint32_t sbits[kRows], zbits[kRows];
-      load_rows(j, cb, sbits, zbits);
-      consume(X, cb, sbits, zbits);
-    }
-  }
+    } else {
+      const uint32_t goff = (uint32_t)(j / kBlocksPerGroup);
 #pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-    const float v = wave_sum(yacc[r]);
-    if (lane == 63) partial[wave][r] = v;
+      for (int r = 0; r < kRows; ++r) {
+        sbits[r] = __builtin_amdgcn_raw_buffer_load_b16(rs, live ? (r * groups_per_row + goff) * 2 : kOutOfRange, 0, 0);
+        zbits[r] = ZP ? __builtin_amdgcn_raw_buffer_load_b8(rz, live ? r * groups_per_row + goff : kOutOfRange, 0, 0) : 0u;
+      }
+    }
+    Block<Q> cb[kRows];
+#pragma unroll
+    for (int r = 0; r < kRows; ++r)
+      buffer_block_codes<Q>(rc, live ? r * row_bytes + (uint32_t)j * (4 * Q) : kOutOfRange, 0, cb[r].d);
+
+    // Through LDS: chunk c = 64 i + lane of the pass is piece c % 4 of block c / 4.
+    wave_sync_lds();   // the previous pass's reads are done
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xw[x_slot(16 * i + (lane >> 2), lane & 3)] = xq[i];
+    if constexpr (VS) {
+      if (lane < S::kScaleChunks) xw[kXChunks + lane] = sq;
+      if constexpr (ZP) if (lane < S::kZpChunks) xw[kXChunks + S::kScaleChunks + lane] = zq;
+    }
+    wave_sync_lds();
+    uint32_t X[16];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const u32x4 v = xw[x_slot(lane, p)];
+      X[4 * p] = v.x; X[4 * p + 1] = v.y; X[4 * p + 2] = v.z; X[4 * p + 3] = v.w;
+    }
+    if constexpr (VS) {
+      const int g = lane / kBlocksPerGroup;
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        sbits[r] = *reinterpret_cast<const uint16_t*>(sw + r * S::kScaleBytes + 2 * g);
+        zbits[r] = ZP ? zw[r * S::kZpBytes + g] : 0u;
+      }
+    }
+    consume(X, cb, sbits, zbits);
+  }
+  // Four row sums at once: swapping lane halves (32 apart, then 16 apart) folds the
+  // four values of a lane into one, leaving in 16-lane row R the partials of row
+  // (R & 1) * 2 + (R >> 1); four DPP steps then finish each 16-lane row.
+  static_assert(kRows == 4, "the folded reduction handles four rows");
+  {
+    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[0]), __float_as_uint(yacc[1]), false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[2]), __float_as_uint(yacc[3]), false, false);
+    const float s01 = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const float s23 = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+    const auto c = __builtin_amdgcn_permlane16_swap(__float_as_uint(s01), __float_as_uint(s23), false, false);
+    float v = __uint_as_float(c[0]) + __uint_as_float(c[1]);
+    v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1,0,3,2]
+    v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2,3,0,1]
+    v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
+    v = dpp_add<0x140, 0xF>(v);   // row_mirror
+    if ((lane & 15) == 0) partial[wave][((lane >> 4) & 1) * 2 + (lane >> 5)] = v;
   }
   __syncthreads();
-  if (t < kRows) {
-    const int64_t row = row0 + t;
-    if (row < N) {
-      const int waves_per_team = team_threads / 64;
-      float v = 0.0f;
-      for (int w = 0; w < waves_per_team; ++w) v += partial[team * waves_per_team + w][t];
-      y[row] = f32_to_bf16_bits(v);
-    }
+  if ((int)threadIdx.x < rows_here) {
+    const int waves = threads >> 6;
+    float v = 0.0f;
+    for (int w = 0; w < waves; ++w) v += partial[w][threadIdx.x];
+    y[row0 + threadIdx.x] = f32_to_bf16_bits(v);
   }
 }
 
@@ -260,13 +338,21 @@ __global__ __launch_bounds__(256) void matmul_f32_kernel(const float* __restrict
 template <int Q, int G, bool ZP>
 hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
                          const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+  using S = Stage<G, ZP>;
   const int64_t nblk = K / 32;
-  const int team = (int)std::min<int64_t>(1024, (nblk + 63) / 64 * 64);
-  const int teams = team >= 256 ? 1 : 256 / team;
-  const int64_t rows_per_block = (int64_t)teams * kRows;
-  const dim3 grid((unsigned)((N + rows_per_block - 1) / rows_per_block));
-  gemv_kernel<Q, G, ZP><<<grid, team * teams, 0, stream>>>(x, codes, scales, zp, (int)N, (int)K,
-                                                           team, y);
+  const int64_t passes = (nblk + kMaxTeam - 1) / kMaxTeam;
+  const int threads = (int)(((nblk + passes - 1) / passes + 63) / 64 * 64);
+  const dim3 grid((unsigned)((N + kRows - 1) / kRows));
+  const size_t lds = (size_t)(threads / 64) * S::kWaveBytes;
+  // One load per wavefront covers the rows' scales (and zero points) when every row's
+  // run of them starts 16-byte aligned.
+  const int64_t groups = K / G;
+  const bool vs = reinterpret_cast<uintptr_t>(scales) % 16 == 0 && (groups * 2) % 16 == 0 &&
+                  (!ZP || (reinterpret_cast<uintptr_t>(zp) % 16 == 0 && groups % 16 == 0));
+  if (vs)
+    gemv_kernel<Q, G, ZP, true><<<grid, threads, lds, stream>>>(x, codes, scales, zp, (int)N, (int)K, y);
+  else
+    gemv_kernel<Q, G, ZP, false><<<grid, threads, lds, stream>>>(x, codes, scales, zp, (int)N, (int)K, y);
   return hipGetLastError();
 }
 

@@ -85,6 +85,39 @@ def test_gemv_odd_reduction_lengths(K):
         check_matmul(w, x, 32, 4, mode, tag=f"gemv K={K}")
 
 
+@pytest.mark.parametrize("q,group", [(4, 32), (3, 64), (2, 128)])
+def test_gemv_multi_pass_ragged(q, group):
+    # K=17408 is 544 blocks: two passes of a 320-thread team, the second one partial.
+    K = 17408
+    w = rand_w(21, K, seed=q + group)
+    x = synth.activations(1, K, seed=5)
+    for mode in MODES:
+        check_matmul(w, x, group, q, mode, tag=f"gemv multi-pass q={q} g={group}")
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_gemv_unaligned_metadata(mode):
+    """Scales (and zero points) that start off a 16-byte boundary take the per-lane
+    load path; the result equals the aligned call bit for bit."""
+    N, K = 24, 2048
+    w = rand_w(N, K, seed=3)
+    codes, scales, zp = ssq.ssq_quantize(to_device(w, True), 32, 4, mode)
+    X = to_device(synth.activations(1, K, seed=4), True)
+    y_ref = ssq.ssq_matmul(X, codes, scales, zp, N, K, 32, 4)
+    s_buf = torch.zeros(scales.numel() + 8, dtype=scales.dtype, device="cuda")
+    s_off = s_buf[1:1 + scales.numel()].view(scales.shape)
+    s_off.copy_(scales)
+    z_off = None
+    if zp is not None:
+        z_buf = torch.zeros(zp.numel() + 16, dtype=zp.dtype, device="cuda")
+        z_off = z_buf[3:3 + zp.numel()].view(zp.shape)
+        z_off.copy_(zp)
+    assert s_off.data_ptr() % 16 != 0
+    y = ssq.ssq_matmul(X, codes, s_off, z_off, N, K, 32, 4)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y_ref)
+
+
 @pytest.mark.parametrize("q", [2, 3, 4])
 @pytest.mark.parametrize("group", [32, 128])
 @pytest.mark.parametrize("mode", MODES)
