@@ -214,19 +214,18 @@ template <int Q, int G, bool ZP, int MB>
 __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
     const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
     const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zp, int N, int K,
-    uint16_t* __restrict__ y, int splits, float* __restrict__ partials,
+    uint16_t* __restrict__ y, int splits, int per, float* __restrict__ partials,
     unsigned int* __restrict__ counters) {
   constexpr int kStage = MB * 16 * 128 * 2;    // MB*16 tokens x 128 k, bf16
   __shared__ __attribute__((aligned(1024))) uint8_t xs[kChunk * kStage];
   __shared__ unsigned int arrived;
 
+  // Grid: x = row block, y = slice of K (`per` super-blocks each).
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int row_blocks = (N + kSplitRows - 1) / kSplitRows;
-  const int rb = (int)blockIdx.x % row_blocks, split = (int)blockIdx.x / row_blocks;
+  const int rb = (int)blockIdx.x, split = (int)blockIdx.y;
   const int64_t n0 = (int64_t)rb * kSplitRows + wave * 16;      // this wavefront's rows
   const int nblk = K / 32, nsb = (nblk + 3) / 4;
-  const int per = (nsb + splits - 1) / splits;
   const int sb_begin = std::min(nsb, split * per);
   const int nsteps = std::min(nsb, sb_begin + per) - sb_begin;
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
@@ -330,12 +329,18 @@ __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
   if (splits > 1) {
     // Same protocol as the split GEMM: write-through partials, arrival count, the last
     // workgroup of the row block sums the slices in slice order and resets the count.
-    float* mine = partials + (((int64_t)rb * splits + split) * kSplitWaves + wave) * (MB * 256) + lane;
+    // Partials: [row block][slice][wavefront][token block][lane] x 4 floats, stored and
+    // loaded 16 bytes per lane with device-scope coherence (sc1: written through to
+    // memory, read past the non-coherent L2).
+    constexpr int kSc1 = 16;
+    constexpr uint32_t kSliceBytes = kSplitWaves * MB * 256 * 4;
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(partials + (int64_t)rb * splits * (kSliceBytes / 4),
+                                                (uint32_t)splits * kSliceBytes);
+    const uint32_t mine = (uint32_t)wave * (MB * 1024) + (uint32_t)lane * 16;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        __hip_atomic_store(mine + mb * 256 + r * 64, acc[mb][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[mb]), rp,
+                                             (uint32_t)split * kSliceBytes + mine + mb * 1024, 0, kSc1);
     wait_vmcnt<0>();
     __syncthreads();
     if (tid == 0) arrived = atomicAdd(&counters[rb], 1u);
@@ -343,24 +348,26 @@ __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
     if (arrived != (unsigned int)(splits - 1)) return;
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    // Eight slices per round trip: all loads of a round are issued before any add (a
+    // Sixteen slices per round trip: all loads of a round are issued before any add (a
     // slice index past the count reloads slice 0 and is added as zero).
-    constexpr int kBatch = 8;
-    const float* base = partials + ((int64_t)rb * splits * kSplitWaves + wave) * (MB * 256) + lane;
+    constexpr int kBatch = 16;
     for (int o0 = 0; o0 < splits; o0 += kBatch) {
-      float v[kBatch][MB * 4];
+      f32x4 v[kBatch][MB];
 #pragma unroll
       for (int i = 0; i < kBatch; ++i) {
-        const int o = o0 + i < splits ? o0 + i : 0;
-        const float* part = base + (int64_t)o * kSplitWaves * (MB * 256);
+        const uint32_t o = o0 + i < splits ? (uint32_t)(o0 + i) : 0u;
 #pragma unroll
-        for (int e = 0; e < MB * 4; ++e)
-          v[i][e] = __hip_atomic_load(part + (e >> 2) * 256 + (e & 3) * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int mb = 0; mb < MB; ++mb)
+          v[i][mb] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, o * kSliceBytes + mine + mb * 1024, 0, kSc1));
       }
 #pragma unroll
-      for (int i = 0; i < kBatch; ++i)
+      for (int i = 0; i < kBatch; ++i) {
+        const bool live = o0 + i < splits;
 #pragma unroll
-        for (int e = 0; e < MB * 4; ++e) acc[e >> 2][e & 3] += o0 + i < splits ? v[i][e] : 0.0f;
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[mb][e] += live ? v[i][mb][e] : 0.0f;
+      }
     }
     if (tid == 0) __hip_atomic_store(&counters[rb], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -382,13 +389,15 @@ hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, c
   if (p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace) {
     unsigned int* counters = static_cast<unsigned int*>(workspace);
     float* partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + split_counter_bytes(p.row_blocks));
-    const dim3 grid((unsigned)(p.row_blocks * p.splits)), block(64 * kSplitWaves);
+    const int64_t nsb = (K / 32 + 3) / 4;
+    const int per = (int)((nsb + p.splits - 1) / p.splits);
+    const dim3 grid((unsigned)p.row_blocks, (unsigned)p.splits), block(64 * kSplitWaves);
     if (p.mb == 1)
       skinny_split_kernel<Q, G, ZP, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
-                                                                   y, p.splits, partials, counters);
+                                                                   y, p.splits, per, partials, counters);
     else
       skinny_split_kernel<Q, G, ZP, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
-                                                                   y, p.splits, partials, counters);
+                                                                   y, p.splits, per, partials, counters);
     return hipGetLastError();
   }
   const int64_t nsb = (K / 32 + 3) / 4;
