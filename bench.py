@@ -22,6 +22,9 @@ its launches.  ``value`` is the decode GEMV's algorithmic HBM bandwidth (codes
 TFLOP/s and the quantize kernel's bandwidth are reported beside it.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+       python bench.py --sweep      (format sweep: all Llama3-8B projections at every
+                                     q, g and mode; the prefill GEMM per mode; the
+                                     Llama3-70B block at q=2 -- one JSON line)
 """
 from __future__ import annotations
 
@@ -61,9 +64,11 @@ KERNEL_SOURCES = {
 }
 
 
-def measured_traffic(kind: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or None if absent
-    or taken on a different version of the kernel's source."""
+def measured_traffic(kind: str, mode: str = "signed_sym"):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None if absent,
+    taken on a different version of the kernel's source, or on another mode."""
+    if mode != "signed_sym":
+        return None
     try:
         with open(TRAFFIC_FILE) as f:
             data = json.load(f)
@@ -86,6 +91,8 @@ def parse_args():
     p.add_argument("--mode", choices=["signed_sym", "unsigned_sym", "asym"], default="signed_sym")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--batched-m", type=int, default=16, help="tokens of the batched-decode phase")
+    p.add_argument("--sweep", action="store_true",
+                   help="format sweep over the Llama3 shapes instead of the headline step")
     p.add_argument("--phases", default="quantize,gemv,batched,gemm",
                    help="comma list of phases to run (profiling runs isolate one kernel); "
                         "'copy' adds a plain 256 MiB device copy used to calibrate byte counters")
@@ -141,12 +148,159 @@ def cpu_baseline(w_bits: np.ndarray, x_bits: np.ndarray, N: int, K: int, g: int,
     }
 
 
+SWEEP_MODES = ("signed_sym", "unsigned_sym", "asym")
+HBM_TARGET_BYTES = 600 << 20    # distinct weight bytes per timed pass: over twice the Infinity Cache
+
+
+def _graph_time(torch, fn, reps: int) -> float:
+    """Seconds per replay of a HIP graph holding the launches fn() makes."""
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            g.replay()
+        e1.record(s)
+        torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1e3 / reps
+
+
+def _eager_time(torch, fn, reps: int) -> float:
+    """Seconds per call of fn() launched eagerly on the null stream (ssq_quantize's stream)."""
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1e3 / reps
+
+
+def matmul_bytes(M, N, K, q, g, asym):
+    return N * K * q // 8 + 2 * N * K // g + (N * K // g if asym else 0) + 2 * M * K + 2 * M * N
+
+
+def quantize_bytes(N, K, q, g, asym):
+    return 2 * N * K + N * K * q // 8 + 2 * N * K // g + (N * K // g if asym else 0)
+
+
+def sweep(args) -> int:
+    """Throughput of every format on the Llama3 shapes (event-timed; weights past the
+    Infinity Cache for the decode passes).  One JSON line with a row per case."""
+    import torch
+
+    from paper_2607_08779_amd import ssq, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    t_start = time.perf_counter()
+
+    def dev_bf16(a):
+        return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    rows = []
+
+    def block_pass(wl, names, q, g, mode_name, ms):
+        """Quantize the block (its launches in sequence), then matmuls at each M through
+        enough quantized copies of the block to stream from HBM."""
+        mode = ssq.MODES[mode_name]
+        asym = mode == ssq.ASYM
+        shapes = {n: (wl.layers[n].rows, wl.layers[n].cols) for n in names}
+        first = {n: ssq.ssq_quantize(W[n], g, q, mode) for n in names}
+        t_q = _eager_time(torch, lambda: [ssq.ssq_quantize(W[n], g, q, mode, out=first[n]) for n in names], 5)
+        qb = sum(quantize_bytes(N, K, q, g, asym) for N, K in shapes.values())
+        rows.append({"block": wl.name, "op": "quantize", "q": q, "group": g, "mode": mode_name,
+                     "launches": len(names), "us": round(t_q * 1e6, 2), "bytes": qb,
+                     "gbs": round(qb / t_q / 1e9, 1), "frac_hbm": round(qb / t_q / 1e9 / HBM_PEAK_GBS, 4)})
+        wbytes = sum(matmul_bytes(0, N, K, q, g, asym) for N, K in shapes.values())
+        copies = [first] + [{n: ssq.ssq_quantize(W[n], g, q, mode) for n in names}
+                            for _ in range(max(0, -(-HBM_TARGET_BYTES // wbytes) - 1))]
+        for M in ms:
+            xs = {K: dev_bf16(synth.activations(M, K, seed=wl.x_seed + M)) for _, K in shapes.values()}
+            ys = {n: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for n, (N, K) in shapes.items()}
+            wss = {n: ssq.ssq_matmul_workspace(M, N, K, g, q, device=dev) for n, (N, K) in shapes.items()}
+
+            def run():
+                for c in copies:
+                    for n in names:
+                        N, K = shapes[n]
+                        ssq.ssq_matmul(xs[K], *c[n], N, K, g, q, out=ys[n], workspace=wss[n])
+
+            t = _graph_time(torch, run, 10) / len(copies)
+            mb = sum(matmul_bytes(M, N, K, q, g, asym) for N, K in shapes.values())
+            fl = sum(2 * M * N * K for N, K in shapes.values())
+            rows.append({"block": wl.name, "op": f"matmul M={M}", "q": q, "group": g, "mode": mode_name,
+                         "launches": len(names), "copies": len(copies), "us": round(t * 1e6, 2),
+                         "bytes": mb, "gbs": round(mb / t / 1e9, 1),
+                         "frac_hbm": round(mb / t / 1e9 / HBM_PEAK_GBS, 4),
+                         "tflops": round(fl / t / 1e12, 2)})
+        del copies, first
+        torch.cuda.empty_cache()
+
+    # Llama3-8B block: q in {2,3,4}, g in {32,64,128}, three modes; decode GEMV (M=1).
+    wl = synth.llama3_8b_block()
+    names = list(synth.LLAMA3_8B)
+    W = {n: dev_bf16(synth.weights(wl.layers[n])) for n in names}
+    for q in (2, 3, 4):
+        for g in (32, 64, 128):
+            for mode_name in SWEEP_MODES:
+                block_pass(wl, names, q, g, mode_name, (1,))
+
+    # Prefill GEMM (W4 g32) on both MLP orientations, per mode.
+    pf = synth.prefill()
+    for n, spec in pf.layers.items():
+        Wp = dev_bf16(synth.weights(spec))
+        N, K = spec.rows, spec.cols
+        for mode_name in SWEEP_MODES:
+            mode = ssq.MODES[mode_name]
+            c, s_, z = ssq.ssq_quantize(Wp, 32, 4, mode)
+            for M in (512, 2048):
+                x = dev_bf16(synth.activations(M, K, seed=pf.x_seed + M))
+                y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+                ws = ssq.ssq_matmul_workspace(M, N, K, 32, 4, device=dev)
+                t = _graph_time(torch, lambda: [ssq.ssq_matmul(x, c, s_, z, N, K, 32, 4, out=y, workspace=ws)
+                                                for _ in range(4)], 5) / 4
+                tf = 2 * M * N * K / t / 1e12
+                rows.append({"block": pf.name, "op": f"gemm {n} M={M}", "q": 4, "group": 32,
+                             "mode": mode_name, "N": N, "K": K, "us": round(t * 1e6, 2),
+                             "tflops": round(tf, 2), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4)})
+        del Wp
+    del W
+    torch.cuda.empty_cache()
+
+    # Llama3-70B block at q=2, g=32: quantize, then M=1 and M=16 per mode.
+    wl = synth.llama3_70b_block()
+    names = list(synth.LLAMA3_70B)
+    W = {n: dev_bf16(synth.weights(wl.layers[n])) for n in names}
+    for mode_name in SWEEP_MODES:
+        block_pass(wl, names, 2, 32, mode_name, (1, 16))
+    del W
+    torch.cuda.empty_cache()
+
+    print(json.dumps({"sweep": "format sweep on synthetic Llama3 shapes", "data": "synthetic",
+                      "hbm_peak_gbs": HBM_PEAK_GBS, "bf16_peak_tflops": BF16_PEAK_TFLOPS,
+                      "wall_s": round(time.perf_counter() - t_start, 1), "rows": rows}), flush=True)
+    return 0
+
+
 def main() -> int:
     args = parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         return 2
+    if args.sweep:
+        return sweep(args)
     import torch
 
     from paper_2607_08779_amd import ssq, synth
@@ -298,7 +452,7 @@ def main() -> int:
         out["value"] = round(gbs, 2)
         out["roofline"] = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
                            "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                           "traffic": measured_traffic("gemv"),
+                           "traffic": measured_traffic("gemv", args.mode),
                            "kernel": "gemv_kernel (ssq_matmul, M=1)",
                            "bytes_per_launch": gemv_bytes, "avg_launch_us": round(avg * 1e6, 3)}
     if "batched" in phases:
@@ -307,7 +461,7 @@ def main() -> int:
         out["batched_decode_gbs"] = round(gbs, 2)
         out["roofline_batched"] = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
                                    "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                   "traffic": measured_traffic("batched"),
+                                   "traffic": measured_traffic("batched", args.mode),
                                    "kernel": f"skinny_split_kernel (ssq_matmul, M={args.batched_m})",
                                    "bytes_per_launch": batched_bytes, "avg_launch_us": round(avg * 1e6, 3),
                                    "tflops": round(2 * args.batched_m * N * K / avg / 1e12, 2)}
@@ -318,7 +472,7 @@ def main() -> int:
         out["roofline_gemm"] = {"bound": "mfma", "achieved": round(tf, 2),
                                 "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                 "frac": round(tf / BF16_PEAK_TFLOPS, 4),
-                                "traffic": measured_traffic("gemm"),
+                                "traffic": measured_traffic("gemm", args.mode),
                                 "kernel": f"gemm_kernel (ssq_matmul, M={args.gemm_m})",
                                 "flops_per_launch": gemm_flops, "avg_launch_us": round(avg * 1e6, 3)}
     if "quantize" in phases:
@@ -328,7 +482,7 @@ def main() -> int:
         out["roofline_quantize"] = {"bound": "hbm", "achieved": round(gbs, 2),
                                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
                                     "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                    "traffic": measured_traffic("quantize"),
+                                    "traffic": measured_traffic("quantize", args.mode),
                                     "kernel": "quantize_kernel (ssq_quantize)",
                                     "bytes_per_launch": quant_bytes,
                                     "avg_launch_us": round(avg * 1e6, 3)}
