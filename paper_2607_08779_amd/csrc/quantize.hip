@@ -147,10 +147,35 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
       const float mn0 = fminf(-nmn, 0.0f);
       const float s = (mx0 - mn0) / kTop;
       if (s != 0.0f) {
-        const float z = fminf(fmaxf(rintf(-mn0 / s), 0.0f), kTop);
+        // rint(fl32(a/s)) without a division, for the zero point (a = -mn0) and every
+        // weight (a = w).  0 lies in [mn0, mx0], so |a| <= mx0 - mn0 and
+        // |a/s| < 2^q - 1 + 2^-16 < 16.  With r = rcp(s) (within 1 ulp of 1/s; s is
+        // normal and far from overflow), t = a*r is within 0.75 * 2^-18 of a/s, and
+        // fl32(a/s) within 2^-21 of a/s, so fl32(a/s) lies within 2^-18 of t.  When t is
+        // farther than 2^-18 from every half-integer (|t - rint(t)| < 1/2 - 2^-18, an
+        // exact difference), rint(t) is rint(fl32(a/s)).  Otherwise the half-integer h
+        // next to t decides: if h*s == a exactly (one fma, which cannot underflow for
+        // s >= 2^-100) the quotient is h itself, else the value is divided.  Exact
+        // half-integer quotients are common with bf16 weights (~0.2 % of weights); those
+        // and the rarer near misses branch.
+        const bool fast = s >= 0x1p-100f && s <= 0x1p100f;
+        const float r = __builtin_amdgcn_rcpf(s);
+        auto rint_quotient = [&](float a) {
+          const float t = a * r;
+          float c = rintf(t);
+          if (!fast || __builtin_fabsf(t - c) >= 0.5f - 0x1p-18f) {
+            const float h = t > c ? c + 0.5f : c - 0.5f;
+            c = fast && __builtin_fmaf(h, s, -a) == 0.0f ? rintf(h) : rintf(a / s);
+          }
+          return c;
+        };
+        const float z = fminf(fmaxf(rint_quotient(-mn0), 0.0f), kTop);
+        float rq[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) rq[i] = rint_quotient(w[u][i]);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const float c = fminf(fmaxf(rintf(w[u][i] / s) + z, 0.0f), kTop);
+          const float c = fminf(fmaxf(rq[i] + z, 0.0f), kTop);
           packed |= (uint32_t)(int)c << (Q * i);
         }
         zero_point = (uint8_t)(int)z;

@@ -79,6 +79,11 @@ def _edge_matrix():
     rows.append(-pos)
     one = np.zeros(128, np.float32); one[::32] = -3.0
     rows.append(one)                                       # single negative outlier
+    # min-max grid with s = (0.4375 + 0.5)/15 = 1/16 exactly: every w = (k + 1/2)/16 sits
+    # exactly on a half-integer quotient (the asymmetric quantizer's tie path)
+    half = ((rng.integers(-8, 7, 128) + 0.5) / 16).astype(np.float32)
+    half[::32] = -0.5; half[1::32] = 0.4375
+    rows.append(half)
     return synth.to_bf16_bits(np.stack(rows))
 
 
