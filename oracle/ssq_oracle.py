@@ -17,6 +17,9 @@ The oracle is written to be read against the paper (Colbert, Dash et al.,
 * App. B.1 (formats table): one fp16 scale per 32-weight block, packed few-bit
   indices, no zero point for the symmetric formats.
 * App. B.3 (zero-point cost): Y_ik = sum_b s_kb sum_{j in b} X_ij (Wq_kj - z_kb).
+* App. B.1 (Q4_1 / Q2_1 rows of the formats table): the min-max grid stored as an
+  fp16 scale s and an fp16 minimum m per block, so that a weight reads back as
+  s*u + m (the real zero point z = -min/s of Eq. (2) folded into m = -s*z).
 
 Arithmetic precision.  The paper fixes no precision for the grid computation;
 this oracle computes the scale and the quotient w/s in IEEE binary32 (each
@@ -39,8 +42,10 @@ import numpy as np
 SIGNED_SYM = 0      # signed absmax grid, Eq. (5)
 UNSIGNED_SYM = 1    # absmax grid with s > 0, Eq. (3)
 ASYM = 2            # min-max grid with an integer zero point, Eq. (2)
+ASYM_MIN = 3        # min-max grid with an fp16 minimum, Eq. (2) in the App. B.1 Q*_1 layout
 
-MODE_NAMES = {SIGNED_SYM: "signed_sym", UNSIGNED_SYM: "unsigned_sym", ASYM: "asym"}
+MODE_NAMES = {SIGNED_SYM: "signed_sym", UNSIGNED_SYM: "unsigned_sym", ASYM: "asym",
+              ASYM_MIN: "asym_min"}
 
 READINGS = {
     "tie_break": "Eq. (5) asks for deterministic tie-breaking in argmax|w_i|; when both +M and -M "
@@ -55,6 +60,13 @@ READINGS = {
                        "max(max w, 0)), so z = rne(fl32(-min'/s)) lies in [0, 2^q-1] and the grid "
                        "still covers the data.  Codes are clip(rne(fl32(w/s)) + z, 0, 2^q-1), the "
                        "zero point being added after rounding; an all-zero group stores zeros.",
+    "asym_min": "For the fp16-minimum layout (App. B.1, Q4_1/Q2_1) the grid is Eq. (2) on the "
+                "group's own range (no widening): s = fl32(fl32(max - min)/(2^q-1)), and Eq. (1) "
+                "with the real zero point z = -min/s is evaluated as u = clip(rne(fl32(fl32(w - "
+                "min)/s)), 0, 2^q-1), which equals round(w/s + z) in exact arithmetic.  The "
+                "stored minimum is binary16(min) (half to even); a weight reads back as s*u + m "
+                "with the stored binary16 s and m.  A constant group (max == min) stores s = 0, "
+                "codes 0 and m = binary16(min).",
     "index_encoding": "Symmetric codes c in A_q are stored as the offset-binary index u = c + 2^(q-1).",
     "bit_order": "Field k of a row occupies bits [k*q, k*q+q) of the row's little-endian bit stream.",
 }
@@ -68,6 +80,7 @@ class Quantized(NamedTuple):
     zp: Optional[np.ndarray]          # uint8 [rows, cols/group] for ASYM, else None
     scale32: np.ndarray               # float32 [rows, cols/group], the scale the codes used
     u: np.ndarray                     # int64 [rows, cols], unpacked indices
+    mins: Optional[np.ndarray] = None  # uint16 [rows, cols/group] binary16 minimums for ASYM_MIN
 
 
 # ---------------------------------------------------------------------------
@@ -178,6 +191,20 @@ def quantize(W: np.ndarray, group: int, q: int, mode: int) -> Quantized:
         z = np.where(flat, np.float32(0), z)
         u = c.astype(np.int64).reshape(rows, cols)
         zp = z.astype(np.uint8)
+    elif mode == ASYM_MIN:
+        lo, hi = unsigned_alphabet(q)
+        rng32 = (mx - mn).astype(np.float32)                    # fl32(max - min)
+        s32 = (rng32 / np.float32(hi)).astype(np.float32)       # Eq. (2): s = (max-min)/(2^q-1)
+        flat = s32 == 0                                         # constant group
+        safe_s = np.where(flat, np.float32(1), s32)
+        d = (G - mn[..., None]).astype(np.float32)              # fl32(w - min) >= 0
+        t = (d / safe_s[..., None]).astype(np.float32)          # fl32((w - min)/s)
+        c = np.clip(np.rint(t), np.float32(lo), np.float32(hi))  # Eq. (1): round(w/s + z), z = -min/s
+        c = np.where(flat[..., None], np.float32(0), c)
+        s32 = np.where(flat, np.float32(0), s32)
+        u = c.astype(np.int64).reshape(rows, cols)
+        return Quantized(codes=pack(u, q), scales=f16_bits_from_f32(s32), zp=None,
+                         scale32=s32.astype(np.float32), u=u, mins=f16_bits_from_f32(mn))
     else:
         raise ValueError(f"unknown mode {mode}")
 
@@ -220,27 +247,32 @@ def unpack(codes: np.ndarray, cols: int, q: int) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 def dequantize(codes: np.ndarray, scales: np.ndarray, zp: Optional[np.ndarray],
-               cols: int, group: int, q: int) -> np.ndarray:
+               cols: int, group: int, q: int, mins: Optional[np.ndarray] = None) -> np.ndarray:
     """W_hat[n, k] = s[n, b] * (u[n, k] - o[n, b]) in binary64, b = k // group.
 
     o = 2^(q-1) for the symmetric formats (the index offset) and o = zp for the
-    asymmetric one, i.e. Eq. (1) read back with the stored binary16 scale.
+    asymmetric one, i.e. Eq. (1) read back with the stored binary16 scale.  With
+    ``mins`` (the App. B.1 Q*_1 layout) W_hat = s*u + m instead.
     """
     u = unpack(codes, cols, q).astype(np.float64)
     rows = u.shape[0]
     s = f16_bits_to_f64(scales).reshape(rows, cols // group, 1)
+    ug = u.reshape(rows, cols // group, group)
+    if mins is not None:
+        m = f16_bits_to_f64(mins).reshape(rows, cols // group, 1)
+        return (s * ug + m).reshape(rows, cols)
     if zp is None:
         o = np.float64(1 << (q - 1))
     else:
         o = np.asarray(zp, dtype=np.float64).reshape(rows, cols // group, 1)
-    return (s * (u.reshape(rows, cols // group, group) - o)).reshape(rows, cols)
+    return (s * (ug - o)).reshape(rows, cols)
 
 
 def matmul(x: np.ndarray, codes: np.ndarray, scales: np.ndarray, zp: Optional[np.ndarray],
-           N: int, K: int, group: int, q: int) -> np.ndarray:
+           N: int, K: int, group: int, q: int, mins: Optional[np.ndarray] = None) -> np.ndarray:
     """y[m, n] = sum_k x[m, k] * W_hat[n, k], evaluated in binary64 (App. B.3)."""
     x64 = np.asarray(x, dtype=np.float64).reshape(-1, K)
-    W_hat = dequantize(codes, scales, zp, K, group, q)
+    W_hat = dequantize(codes, scales, zp, K, group, q, mins)
     if W_hat.shape[0] != N:
         raise ValueError("codes do not have N rows")
     return x64 @ W_hat.T

@@ -19,7 +19,7 @@ import torch
 from oracle import ssq_oracle as O
 from paper_2607_08779_amd import synth
 
-SIGNED, UNSIGNED, ASYM = O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM
+SIGNED, UNSIGNED, ASYM, ASYM_MIN = O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM, O.ASYM_MIN
 
 
 # ---------------------------------------------------------------------------
@@ -87,6 +87,13 @@ def test_worked_example_q2(golden_dir):
         c = codes_of(r, gold["q"], mode)[0]
         err2 = sum((Fr(float(wi)) - s * int(ci)) ** 2 for wi, ci in zip(w[0], c))
         assert abs(float(err2) - exp["err2"]) < 1e-6, name
+    r = O.quantize(w, gold["group"], gold["q"], ASYM_MIN)
+    exp = gold["asym_min"]
+    assert r.u[0].tolist() == exp["u"] and int(r.codes[0, 0]) == exp["byte"]
+    assert int(r.scales[0, 0]) == exp["scale_bits"] and int(r.mins[0, 0]) == exp["min_bits"]
+    assert r.zp is None
+    back = O.dequantize(r.codes, r.scales, None, 4, 4, 2, mins=r.mins)
+    assert back[0].tolist() == exp["dequant"]
 
 
 def test_rounding_is_half_to_even():
@@ -109,6 +116,8 @@ def test_block_sizes_match_paper(golden_dir):
         r = O.quantize(w, 32, q, ASYM)
         # our asymmetric form stores a u8 zero point instead of the fp16 minimum
         assert r.codes.nbytes + r.scales.nbytes + r.zp.nbytes == gold[f"Q{q}_1"] - 1
+        r = O.quantize(w, 32, q, ASYM_MIN)   # the paper's Q*_1 layout: fp16 s + fp16 m
+        assert r.codes.nbytes + r.scales.nbytes + r.mins.nbytes == gold[f"Q{q}_1"]
 
 
 # ---------------------------------------------------------------------------
@@ -441,6 +450,51 @@ def test_asym_grid_properties(q):
                 assert e <= s / 2 + s * Fr(1, 2 ** 20)
 
 
+@pytest.mark.parametrize("q", [2, 3, 4])
+def test_asym_min_grid_properties(q):
+    """The fp16-minimum layout of Eq. (2): exact-rational checks of every code."""
+    w = np.concatenate([bf16_groups(150, 32, seed=1800 + q), f32_groups(150, 32, seed=1900 + q),
+                        np.abs(f32_groups(40, 32, seed=3)) + 0.5, -np.abs(f32_groups(40, 32, seed=4))])
+    r = O.quantize(w, 32, q, ASYM_MIN)
+    top = 2 ** q - 1
+    n_checked = 0
+    for n, row in enumerate(w):
+        s = Fr(float(r.scale32[n, 0]))
+        mn, mx = Fr(float(row.min())), Fr(float(row.max()))
+        exact_s = (mx - mn) / top
+        assert abs(s - exact_s) <= exact_s * Fr(1, 2 ** 22)       # two binary32 roundings
+        assert int(r.mins[n, 0]) == struct.unpack("<H", struct.pack("<e", float(row.min())))[0]
+        u = r.u[n]
+        assert u[int(np.argmin(row))] == 0 and u[int(np.argmax(row))] == top
+        for k, v in enumerate(row):
+            wv = Fr(float(v))
+            # Eq. (1) with the real zero point z = -min/s, in exact arithmetic
+            t = wv / s + (-mn / s)
+            if near_half(t, Fr(1, 2 ** 18)):
+                continue      # binary32 rounding of w - min and of the quotient may decide
+            assert int(u[k]) == min(max(rne(t), 0), top)
+            # nearest point of the grid {s*v + min}: no clipping inside [min, max]
+            assert abs(wv - (s * int(u[k]) + mn)) <= s / 2 + s * Fr(1, 2 ** 18)
+            n_checked += 1
+    assert n_checked > 10000
+
+
+def test_asym_min_dequantize_reads_s_u_plus_m():
+    """W_hat = s16 * u + m16 from the stored bit patterns (exact rationals)."""
+    w = bf16_groups(20, 32, seed=77)
+    r = O.quantize(w, 32, 4, ASYM_MIN)
+    back = O.dequantize(r.codes, r.scales, None, 32, 32, 4, mins=r.mins)
+    for n in range(20):
+        s16 = Fr(float(struct.unpack("<e", struct.pack("<H", int(r.scales[n, 0])))[0]))
+        m16 = Fr(float(struct.unpack("<e", struct.pack("<H", int(r.mins[n, 0])))[0]))
+        for k in range(32):
+            assert Fr(float(back[n, k])) == s16 * int(r.u[n, k]) + m16
+    # and the matmul is that dequantized matrix times x, in binary64
+    x = np.random.default_rng(5).standard_normal((3, 32))
+    y = O.matmul(x, r.codes, r.scales, None, 20, 32, 32, 4, mins=r.mins)
+    assert np.allclose(y, x @ back.T, rtol=1e-12, atol=0)
+
+
 def test_degenerate_groups():
     q = 4
     w = np.zeros((3, 32), np.float32)
@@ -455,11 +509,14 @@ def test_degenerate_groups():
     assert (r.scales[:2] == 0).all() and (r.zp[:2] == 0).all() and (r.u[:2] == 0).all()
     # constant positive group: range [0, 0.375], z = 0, every index 2^q-1, exact up to s rounding
     assert int(r.zp[2, 0]) == 0 and (r.u[2] == 15).all()
+    r = O.quantize(w, 32, q, ASYM_MIN)     # constant groups: s = 0, codes 0, m = the constant
+    assert (r.scales == 0).all() and (r.u == 0).all()
+    assert [int(b) for b in r.mins[:, 0]] == [0x0000, 0x8000, 0x3600]   # +0, -0, 0.375
 
 
 def test_scale_storage_matches_python_binary16():
     w = f32_groups(64, 32, seed=3)
-    for mode in (SIGNED, UNSIGNED, ASYM):
+    for mode in (SIGNED, UNSIGNED, ASYM, ASYM_MIN):
         r = O.quantize(w, 32, 4, mode)
         for s32, bits in zip(r.scale32.ravel(), r.scales.ravel()):
             assert struct.unpack("<H", struct.pack("<e", float(s32)))[0] == int(bits)
