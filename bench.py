@@ -88,7 +88,7 @@ def parse_args():
     p.add_argument("--layers", type=int, default=16, help="distinct quantized copies (decode depth)")
     p.add_argument("--gemm-layers", type=int, default=4, help="prefill GEMMs per step")
     p.add_argument("--gemm-m", type=int, default=512)
-    p.add_argument("--mode", choices=["signed_sym", "unsigned_sym", "asym"], default="signed_sym")
+    p.add_argument("--mode", choices=["signed_sym", "unsigned_sym", "asym", "asym_min"], default="signed_sym")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--batched-m", type=int, default=16, help="tokens of the batched-decode phase")
     p.add_argument("--sweep", action="store_true",
@@ -118,13 +118,13 @@ def cpu_baseline(w_bits: np.ndarray, x_bits: np.ndarray, N: int, K: int, g: int,
             t0 = time.perf_counter()
             r = O.quantize(O.bf16_bits_to_f32(wf_sample), g, q, mode)
             t1 = time.perf_counter()
-            O.matmul(xf, r.codes, r.scales, r.zp, rows, K, g, q)
+            O.matmul(xf, r.codes, r.scales, r.zp, rows, K, g, q, mins=r.mins)
             t2 = time.perf_counter()
             t_quant += t1 - t0
             t_gemv += t2 - t1
             reps += 1
     gemv_bytes = gemv_bytes_per_row * rows
-    quant_bytes = rows * K * (2 + q / 8 + 2 / g + (1 / g if mode == 2 else 0))
+    quant_bytes = rows * K * (2 + q / 8 + 2 / g + ({2: 1, 3: 2}.get(mode, 0) / g))
     cpu_model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -148,7 +148,7 @@ def cpu_baseline(w_bits: np.ndarray, x_bits: np.ndarray, N: int, K: int, g: int,
     }
 
 
-SWEEP_MODES = ("signed_sym", "unsigned_sym", "asym")
+SWEEP_MODES = ("signed_sym", "unsigned_sym", "asym", "asym_min")
 HBM_TARGET_BYTES = 600 << 20    # distinct weight bytes per timed pass: over twice the Infinity Cache
 
 
@@ -185,12 +185,17 @@ def _eager_time(torch, fn, reps: int) -> float:
     return e0.elapsed_time(e1) / 1e3 / reps
 
 
-def matmul_bytes(M, N, K, q, g, asym):
-    return N * K * q // 8 + 2 * N * K // g + (N * K // g if asym else 0) + 2 * M * K + 2 * M * N
+def meta_bytes_per_group(mode_name):
+    """Bytes stored per group beside the scale: u8 zero point, fp16 minimum, or none."""
+    return {"asym": 1, "asym_min": 2}.get(mode_name, 0)
 
 
-def quantize_bytes(N, K, q, g, asym):
-    return 2 * N * K + N * K * q // 8 + 2 * N * K // g + (N * K // g if asym else 0)
+def matmul_bytes(M, N, K, q, g, meta):
+    return N * K * q // 8 + (2 + meta) * N * K // g + 2 * M * K + 2 * M * N
+
+
+def quantize_bytes(N, K, q, g, meta):
+    return 2 * N * K + N * K * q // 8 + (2 + meta) * N * K // g
 
 
 def sweep(args) -> int:
@@ -214,7 +219,7 @@ def sweep(args) -> int:
         """Quantize the block (its launches in sequence), then matmuls at each M through
         enough quantized copies of the block to stream from HBM."""
         mode = ssq.MODES[mode_name]
-        asym = mode == ssq.ASYM
+        asym = meta_bytes_per_group(mode_name)
         shapes = {n: (wl.layers[n].rows, wl.layers[n].cols) for n in names}
         first = {n: ssq.ssq_quantize(W[n], g, q, mode) for n in names}
         t_q = _eager_time(torch, lambda: [ssq.ssq_quantize(W[n], g, q, mode, out=first[n]) for n in names], 5)
@@ -324,7 +329,6 @@ def main() -> int:
 
     W = dev_bf16(w_bits)
     x1, xm, xb = dev_bf16(x1_bits), dev_bf16(xm_bits), dev_bf16(xb_bits)
-    zp_on = mode == ssq.ASYM
     layers = []
     for _ in range(args.layers):
         layers.append(ssq.ssq_quantize(W, g, q, mode))
@@ -423,7 +427,7 @@ def main() -> int:
     t_m = sum(e[3].elapsed_time(e[4]) for e in events) / 1e3
     t_step = sum(e[0].elapsed_time(e[4]) for e in events) / 1e3 / args.steps
 
-    zp_bytes = N * K // g if zp_on else 0
+    zp_bytes = meta_bytes_per_group(args.mode) * N * K // g
     gemv_bytes = N * K * q // 8 + 2 * N * K // g + zp_bytes + 2 * K + 2 * N
     quant_bytes = 2 * N * K + N * K * q // 8 + 2 * N * K // g + zp_bytes
     gemm_flops = 2 * args.gemm_m * N * K

@@ -6,7 +6,7 @@
  * Method: Colbert, Dash et al., "Signed Symmetric Quantization for Few-Bit
  * Integers".  Argument names follow the paper's notation: q (bit width),
  * group (g, the number of consecutive weights sharing one scale), scales (s),
- * zp (z, the zero point).
+ * zp (z, the zero point), mins (m, the group minimum of the Q*_1 layout).
  *
  * Storage format (shared by every entry point)
  * ---------------------------------------------
@@ -20,16 +20,20 @@
  *                                  per group (App. B.1: the Q*_0 formats store
  *                                  s = gamma*alpha, which may be negative).
  *   zp     [rows, cols/group] u8   integer zero point, asymmetric mode only.
+ *   mins   [rows, cols/group] u16  IEEE binary16 group minimum m, the *_min
+ *                                  entry points only (App. B.1: the Q*_1 blocks
+ *                                  store an fp16 scale and an fp16 minimum).
  *
  *   Symmetric modes store the offset-binary index u = c + 2^(q-1) of the code
  *   c in A_q = {-2^(q-1), ..., 2^(q-1)-1}; the weight is s*(u - 2^(q-1)).
  *   The asymmetric mode stores u in {0, ..., 2^q-1}; the weight is s*(u - z).
+ *   The minimum layout stores u in {0, ..., 2^q-1}; the weight is s*u + m.
  *
  * Conventions
  *   - Every pointer is a device pointer owned by the caller.  The library
  *     allocates nothing, frees nothing and keeps no pointer after returning;
  *     scratch memory, where a path can use it, is a caller-provided workspace.
- *   - W, x, y and codes must be 16-byte aligned; scales 2-byte aligned.
+ *   - W, x, y and codes must be 16-byte aligned; scales and mins 2-byte aligned.
  *   - bf16 and fp16 tensors are passed as their uint16_t bit patterns.
  *   - Inputs must be finite; NaN/Inf inputs give unspecified codes.
  *   - Arguments are validated on the host before any launch.  On an error
@@ -130,8 +134,9 @@ int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_
  * ssq_matmul_workspace_size -- bytes of workspace that let ssq_matmul_ws split
  * the reduction of an M x N x K product across workgroups (App. B.3 sums over
  * blocks of K, so disjoint block ranges can be reduced separately and added).
- * Returns 0 when splitting would not help (enough output tiles already, or
- * M <= 32, which never uses the tiled kernel) or the arguments are invalid.
+ * Returns 0 when splitting would not help (M = 1, or enough output tiles
+ * already) or the arguments are invalid.  2 <= M <= 32 sizes the batched-decode
+ * kernel's split, larger M the tiled kernel's.
  */
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q);
 
@@ -157,6 +162,48 @@ int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint
 int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                    const uint8_t* zp, int64_t N, int64_t K, int group, int q, float* y,
                    hipStream_t stream);
+
+/*
+ * The min-max grid in the layout of App. B.1's Q4_1 / Q2_1 rows: an fp16 scale and
+ * an fp16 minimum per group (20 bytes per 32 weights at q=4, 12 at q=2), the
+ * weight reading back as s*u + m.
+ *
+ * ssq_quantize_min -- per group of `group` consecutive weights w (Eq. (2) on the
+ * group's own range, Eq. (1) with the real zero point z = -min/s):
+ *   s = fl32(fl32(max w - min w) / (2^q - 1)),
+ *   u = clip(rne(fl32(fl32(w - min w) / s)), 0, 2^q-1),
+ *   scales = binary16(s), mins = binary16(min w) (both half to even; a minimum
+ *   that is or rounds to a zero is stored as +0).
+ * A constant group stores s = 0, codes 0 and its value as the minimum.
+ *   W, rows, cols, group, q, codes, scales   as ssq_quantize
+ *   mins   device, u16 [rows, cols/group], written; 2-byte aligned, non-NULL
+ * Enqueued on the null stream.  Returns SSQ_OK or a negative ssq_status.
+ */
+int ssq_quantize_min(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                     uint8_t* codes, uint16_t* scales, uint16_t* mins);
+
+/* ssq_quantize_min for binary32 weights W[rows, cols]; otherwise identical. */
+int ssq_quantize_min_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                         uint8_t* codes, uint16_t* scales, uint16_t* mins);
+
+/*
+ * ssq_matmul_min, ssq_matmul_min_ws, ssq_matmul_min_f32 -- ssq_matmul,
+ * ssq_matmul_ws and ssq_matmul_f32 for weights in the minimum layout:
+ *   What[n, k] = fp32(scales[n, b]) * u[n, k] + fp32(mins[n, b]),   b = k / group,
+ * so each block adds m * sum_{k in b} x[k] to the symmetric product (App. B.3).
+ *   mins   device, u16 [N, K/group] binary16 minimums, 2-byte aligned, non-NULL
+ * Every other argument, the kernels chosen by M, the workspace rules and the
+ * errors are those of the corresponding entry point above.
+ */
+int ssq_matmul_min(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                   const uint16_t* mins, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                   hipStream_t stream);
+int ssq_matmul_min_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                      const uint16_t* mins, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream);
+int ssq_matmul_min_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                       const uint16_t* mins, int64_t N, int64_t K, int group, int q, float* y,
+                       hipStream_t stream);
 
 /* Static description of a status code; never NULL. */
 const char* ssq_strerror(int status);

@@ -64,9 +64,11 @@ READINGS = {
                 "group's own range (no widening): s = fl32(fl32(max - min)/(2^q-1)), and Eq. (1) "
                 "with the real zero point z = -min/s is evaluated as u = clip(rne(fl32(fl32(w - "
                 "min)/s)), 0, 2^q-1), which equals round(w/s + z) in exact arithmetic.  The "
-                "stored minimum is binary16(min) (half to even); a weight reads back as s*u + m "
-                "with the stored binary16 s and m.  A constant group (max == min) stores s = 0, "
-                "codes 0 and m = binary16(min).",
+                "stored minimum is binary16(min) (half to even; a minimum that is or rounds to "
+                "a zero is stored as +0, since -0 and +0 compare equal and either may be the "
+                "group's min); a weight reads back "
+                "as s*u + m with the stored binary16 s and m.  A constant group (max == min) "
+                "stores s = 0, codes 0 and m = binary16(min).",
     "index_encoding": "Symmetric codes c in A_q are stored as the offset-binary index u = c + 2^(q-1).",
     "bit_order": "Field k of a row occupies bits [k*q, k*q+q) of the row's little-endian bit stream.",
 }
@@ -203,8 +205,10 @@ def quantize(W: np.ndarray, group: int, q: int, mode: int) -> Quantized:
         c = np.where(flat[..., None], np.float32(0), c)
         s32 = np.where(flat, np.float32(0), s32)
         u = c.astype(np.int64).reshape(rows, cols)
+        m_bits = f16_bits_from_f32(mn)
+        m_bits = np.where((m_bits & 0x7FFF) == 0, np.uint16(0), m_bits)   # a zero minimum: +0
         return Quantized(codes=pack(u, q), scales=f16_bits_from_f32(s32), zp=None,
-                         scale32=s32.astype(np.float32), u=u, mins=f16_bits_from_f32(mn))
+                         scale32=s32.astype(np.float32), u=u, mins=m_bits.astype(np.uint16))
     else:
         raise ValueError(f"unknown mode {mode}")
 

@@ -104,10 +104,10 @@ Plan plan_for(int64_t M, int64_t N, int64_t K) {
   return p;
 }
 
-template <int Q, int G, bool ZP, int WM>
+template <int Q, int G, int META, int WM>
 __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zp, int N, int K,
+    const uint16_t* __restrict__ scales, const void* __restrict__ meta, int N, int K,
     uint16_t* __restrict__ y, int splits, float* __restrict__ partials,
     unsigned int* __restrict__ counters) {
   using C = Cfg<WM>;
@@ -146,7 +146,9 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   const int nsteps = total_steps - s_begin < per_split ? total_steps - s_begin : per_split;
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
   const uint32_t groups_per_row = (uint32_t)(K / G);
-  constexpr float kSymOffset = (float)(1 << (Q - 1));
+  constexpr bool ZP = META != kMetaNone;
+  constexpr int kMetaSize = meta_size<META>();
+  const uint8_t* const zp = static_cast<const uint8_t*>(meta);
   constexpr int kLoadsPerStep = 4 + 2 + (ZP ? 1 : 0);
 
   // Buffer descriptors relative to the tile's first row; rows past M or N read zeros.
@@ -155,7 +157,8 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(x + m0 * K, rows_a * (uint32_t)K * 2);
   const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + n0 * row_bytes, rows_b * row_bytes);
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + n0 * groups_per_row, rows_b * groups_per_row * 2);
-  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + n0 * groups_per_row : zp, ZP ? rows_b * groups_per_row : 0);
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + n0 * groups_per_row * kMetaSize : zp,
+                                              ZP ? rows_b * groups_per_row * kMetaSize : 0);
 
   // Activation tile: BM/8 wavefront loads of 1 KB straight into LDS, four per wave.
   // Load j fills tile rows 8j..8j+7, lane i writing 16 bytes at 16*i, which is row
@@ -202,13 +205,12 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     for (int i = 0; i < Part<Q, P>::kDwords; ++i) c_reg[slot][i] = d[i];
     const uint32_t gi = (uint32_t)lr * groups_per_row + (uint32_t)(blk / (G / 32));
     s_reg[slot] = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? gi * 2 : 0x80000000u, 0, 0);
-    if constexpr (ZP) z_reg[slot] = __builtin_amdgcn_raw_buffer_load_b8(rz, in ? gi : 0x80000000u, 0, 0);
+    if constexpr (ZP) z_reg[slot] = load_group_meta<META>(rz, gi, in);
   };
   auto store_b = [&](int slot, int stage) {
     const float s = f16_bits_to_f32(s_reg[slot]);
-    const float o = ZP ? (float)z_reg[slot] : kSymOffset;
     uint32_t w[16 / P];
-    dequant_part<Q, P>(c_reg[slot], part, s, -(1024.0f + o) * s, w);   // exact: 11-bit x 11-bit
+    dequant_part<Q, P>(c_reg[slot], part, s, dequant_offset<META, Q>(s, ZP ? z_reg[slot] : 0u), w);
     uint8_t* dst = Bs + stage * kBTileBytes;
 #pragma unroll
     for (int e = 0; e < 4 / P; ++e)
@@ -345,9 +347,9 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
       }
 }
 
-template <int Q, int G, bool ZP>
+template <int Q, int G, int META>
 hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
-                         const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, void* workspace,
+                         const void* zp, int64_t N, int64_t K, uint16_t* y, void* workspace,
                          size_t workspace_bytes, hipStream_t stream) {
   const Plan p = plan_for(M, N, K);
   const bool split = p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace;
@@ -357,10 +359,10 @@ hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, con
                           : nullptr;
   const dim3 grid((unsigned)(p.tiles * splits));
   if (p.wm == 4)
-    gemm_kernel<Q, G, ZP, 4><<<grid, Cfg<4>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
+    gemm_kernel<Q, G, META, 4><<<grid, Cfg<4>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
                                                                    (int)K, y, splits, partials, counters);
   else
-    gemm_kernel<Q, G, ZP, 2><<<grid, Cfg<2>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
+    gemm_kernel<Q, G, META, 2><<<grid, Cfg<2>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
                                                                    (int)K, y, splits, partials, counters);
   return hipGetLastError();
 }
@@ -368,10 +370,10 @@ hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, con
 }  // namespace
 
 hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
-                            const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
+                            const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K,
                             int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
                             hipStream_t stream) {
-  SSQ_DISPATCH_QGZ(gemm_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y,
+  SSQ_DISPATCH_QGM(gemm_dispatch, q, group, meta.kind, x, M, codes, scales, meta.ptr, N, K, y,
                    workspace, workspace_bytes, stream);
 }
 

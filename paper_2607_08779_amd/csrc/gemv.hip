@@ -3,7 +3,9 @@
 // App. B.3 of the paper: with W[n,k] ~ s[n,b] (u[n,k] - o[n,b]) in group b,
 //   y[n] = sum_b s[n,b] * ( sum_{k in b} x[k] u[n,k]  -  o[n,b] sum_{k in b} x[k] ).
 // The symmetric formats (signed or not -- the sign lives in s) have the
-// constant offset o = 2^(q-1); the asymmetric one reads o from zp.
+// constant offset o = 2^(q-1); the asymmetric one reads o from zp.  The Q*_1 layout
+// of App. B.1 stores a minimum m instead (W ~ s*u + m), which contributes
+// m * sum_{k in b} x[k] per block.
 //
 // Streaming design (HBM bound).  The unit of work is a block of 32 consecutive
 // weights of one row: 4q bytes of codes, loaded by one lane with one vector
@@ -131,13 +133,14 @@ constexpr int kMaxWaves = kMaxTeam / 64;
 constexpr int kXChunks = 256;    // 16-byte activation chunks of one pass: 64 blocks x 64 bytes
 constexpr uint32_t kOutOfRange = 0x80000000u;
 
-template <int G, bool ZP>
+template <int G, int META>
 struct Stage {
   static constexpr int kBlocksPerGroup = G / 32;
   static constexpr int kScaleBytes = 128 / kBlocksPerGroup;   // one row's scales for 64 blocks
-  static constexpr int kZpBytes = 64 / kBlocksPerGroup;
+  static constexpr int kMetaSize = META == kMetaZp ? 1 : META == kMetaMin ? 2 : 0;  // bytes per group
+  static constexpr int kZpBytes = 64 / kBlocksPerGroup * kMetaSize;    // one row's metadata
   static constexpr int kScaleChunks = kRows * kScaleBytes / 16;
-  static constexpr int kZpChunks = ZP ? kRows * kZpBytes / 16 : 0;
+  static constexpr int kZpChunks = kRows * kZpBytes / 16;
   static constexpr int kWaveChunks = kXChunks + kScaleChunks + kZpChunks;
   static constexpr int kWaveBytes = kWaveChunks * 16;
   static_assert(kScaleChunks <= 64 && kZpChunks <= 64, "one load instruction per wavefront");
@@ -153,13 +156,16 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int Q, int G, bool ZP, bool VS>
+template <int Q, int G, int META, bool VS>
 __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restrict__ x,
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales,
-                                                        const uint8_t* __restrict__ zp, int N, int K,
+                                                        const void* __restrict__ meta, int N, int K,
                                                         uint16_t* __restrict__ y) {
-  using S = Stage<G, ZP>;
+  using S = Stage<G, META>;
+  constexpr bool ZP = META != kMetaNone;                   // any per-group metadata
+  constexpr int kMetaSize = S::kMetaSize;
+  const uint8_t* const zp = static_cast<const uint8_t*>(meta);
   constexpr int kBlocksPerGroup = S::kBlocksPerGroup;
   constexpr float kSymOffset = kMagicValue + (float)(1 << (Q - 1));
   __shared__ float partial[kMaxWaves][kRows];
@@ -182,7 +188,8 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
   const __amdgpu_buffer_rsrc_t rs =
       make_rsrc(scales + (int64_t)row0 * groups_per_row, (uint32_t)rows_here * groups_per_row * 2);
   const __amdgpu_buffer_rsrc_t rz =
-      make_rsrc(ZP ? zp + (int64_t)row0 * groups_per_row : zp, ZP ? (uint32_t)rows_here * groups_per_row : 0u);
+      make_rsrc(ZP ? zp + (int64_t)row0 * groups_per_row * kMetaSize : zp,
+                ZP ? (uint32_t)rows_here * groups_per_row * kMetaSize : 0u);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
 
   float yacc[kRows];
@@ -200,8 +207,13 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
     for (int r = 0; r < kRows; ++r) {
       const float acc = block_dot<Q>(cb[r], xp, magic);
       const float sc = f16_bits_to_f32(sbits[r]);
-      const float off = ZP ? kMagicValue + (float)zbits[r] : kSymOffset;
-      yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
+      if constexpr (META == kMetaMin) {    // s * sum x u + m * sum x
+        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-kMagicValue, xs, acc), yacc[r]);
+        yacc[r] = __builtin_fmaf(f16_bits_to_f32(zbits[r]), xs, yacc[r]);
+      } else {
+        const float off = META == kMetaZp ? kMagicValue + (float)zbits[r] : kSymOffset;
+        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
+      }
     }
   };
 
@@ -222,8 +234,9 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
       if (lane < S::kScaleChunks) sq = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
       if constexpr (ZP) {
         constexpr int kZPer = S::kZpBytes / 16;
-        const uint32_t zin = (uint32_t)(jw / kBlocksPerGroup) + 16 * (lane % kZPer);
-        const uint32_t zoff = zin < groups_per_row ? (lane / kZPer) * groups_per_row + zin : kOutOfRange;
+        const uint32_t zin = (uint32_t)(jw / kBlocksPerGroup) * kMetaSize + 16 * (lane % kZPer);
+        const uint32_t zoff = zin < groups_per_row * kMetaSize
+                                  ? (lane / kZPer) * groups_per_row * kMetaSize + zin : kOutOfRange;
         if (lane < S::kZpChunks) zq = __builtin_amdgcn_raw_buffer_load_b128(rz, zoff, 0, 0);
       }
     } else {
@@ -231,7 +244,10 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
 #pragma unroll
       for (int r = 0; r < kRows; ++r) {
         sbits[r] = __builtin_amdgcn_raw_buffer_load_b16(rs, live ? (r * groups_per_row + goff) * 2 : kOutOfRange, 0, 0);
-        zbits[r] = ZP ? __builtin_amdgcn_raw_buffer_load_b8(rz, live ? r * groups_per_row + goff : kOutOfRange, 0, 0) : 0u;
+        if constexpr (META == kMetaMin)
+          zbits[r] = __builtin_amdgcn_raw_buffer_load_b16(rz, live ? (r * groups_per_row + goff) * 2 : kOutOfRange, 0, 0);
+        else
+          zbits[r] = ZP ? __builtin_amdgcn_raw_buffer_load_b8(rz, live ? r * groups_per_row + goff : kOutOfRange, 0, 0) : 0u;
       }
     }
     Block<Q> cb[kRows];
@@ -259,7 +275,10 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
 #pragma unroll
       for (int r = 0; r < kRows; ++r) {
         sbits[r] = *reinterpret_cast<const uint16_t*>(sw + r * S::kScaleBytes + 2 * g);
-        zbits[r] = ZP ? zw[r * S::kZpBytes + g] : 0u;
+        if constexpr (META == kMetaMin)
+          zbits[r] = *reinterpret_cast<const uint16_t*>(zw + r * S::kZpBytes + 2 * g);
+        else
+          zbits[r] = ZP ? zw[r * S::kZpBytes + g] : 0u;
       }
     }
     consume(X, cb, sbits, zbits);
@@ -297,11 +316,11 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
 
 constexpr int kF32Tokens = 4;
 
-template <int Q, int G, bool ZP>
+template <int Q, int G, int META>
 __global__ __launch_bounds__(256) void matmul_f32_kernel(const float* __restrict__ x, int M,
                                                          const uint8_t* __restrict__ codes,
                                                          const uint16_t* __restrict__ scales,
-                                                         const uint8_t* __restrict__ zp, int N,
+                                                         const void* __restrict__ meta, int N,
                                                          int K, float* __restrict__ y) {
   const int lane = threadIdx.x & 63;
   const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -314,10 +333,13 @@ __global__ __launch_bounds__(256) void matmul_f32_kernel(const float* __restrict
     const Block<Q> b = load_block<Q>(codes + n * row_bytes + (int64_t)j * (4 * Q));
     const int64_t gi = n * (K / G) + j / (G / 32);
     const float s = f16_bits_to_f32(scales[gi]);
-    const float o = ZP ? (float)zp[gi] : (float)(1 << (Q - 1));
+    // weight = s*u - s*o, or s*u + m for the minimum layout
+    const float so = META == kMetaMin ? f16_bits_to_f32(static_cast<const uint16_t*>(meta)[gi])
+                   : META == kMetaZp ? -s * (float)static_cast<const uint8_t*>(meta)[gi]
+                                     : -s * (float)(1 << (Q - 1));
     float w[32];
 #pragma unroll
-    for (int k = 0; k < 32; ++k) w[k] = s * ((float)field<Q>(b.d, k) - o);   // exact in fp32
+    for (int k = 0; k < 32; ++k) w[k] = __builtin_fmaf(s, (float)field<Q>(b.d, k), so);
 #pragma unroll
     for (int t = 0; t < kF32Tokens; ++t) {
       if (m0 + t >= M) break;
@@ -335,47 +357,48 @@ __global__ __launch_bounds__(256) void matmul_f32_kernel(const float* __restrict
   }
 }
 
-template <int Q, int G, bool ZP>
+template <int Q, int G, int META>
 hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
-                         const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
-  using S = Stage<G, ZP>;
+                         const void* meta, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+  using S = Stage<G, META>;
   const int64_t nblk = K / 32;
   const int64_t passes = (nblk + kMaxTeam - 1) / kMaxTeam;
   const int threads = (int)(((nblk + passes - 1) / passes + 63) / 64 * 64);
   const dim3 grid((unsigned)((N + kRows - 1) / kRows));
   const size_t lds = (size_t)(threads / 64) * S::kWaveBytes;
-  // One load per wavefront covers the rows' scales (and zero points) when every row's
-  // run of them starts 16-byte aligned.
+  // One load per wavefront covers the rows' scales (and zero points or minimums) when
+  // every row's run of them starts 16-byte aligned.
   const int64_t groups = K / G;
   const bool vs = reinterpret_cast<uintptr_t>(scales) % 16 == 0 && (groups * 2) % 16 == 0 &&
-                  (!ZP || (reinterpret_cast<uintptr_t>(zp) % 16 == 0 && groups % 16 == 0));
+                  (S::kMetaSize == 0 ||
+                   (reinterpret_cast<uintptr_t>(meta) % 16 == 0 && (groups * S::kMetaSize) % 16 == 0));
   if (vs)
-    gemv_kernel<Q, G, ZP, true><<<grid, threads, lds, stream>>>(x, codes, scales, zp, (int)N, (int)K, y);
+    gemv_kernel<Q, G, META, true><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
   else
-    gemv_kernel<Q, G, ZP, false><<<grid, threads, lds, stream>>>(x, codes, scales, zp, (int)N, (int)K, y);
+    gemv_kernel<Q, G, META, false><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
   return hipGetLastError();
 }
 
-template <int Q, int G, bool ZP>
+template <int Q, int G, int META>
 hipError_t f32_dispatch(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
-                        const uint8_t* zp, int64_t N, int64_t K, float* y, hipStream_t stream) {
+                        const void* meta, int64_t N, int64_t K, float* y, hipStream_t stream) {
   const dim3 grid((unsigned)((N + 3) / 4), (unsigned)((M + kF32Tokens - 1) / kF32Tokens));
-  matmul_f32_kernel<Q, G, ZP><<<grid, 256, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+  matmul_f32_kernel<Q, G, META><<<grid, 256, 0, stream>>>(x, (int)M, codes, scales, meta, (int)N, (int)K, y);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_gemv_bf16(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
-                            const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                            GroupMeta meta, int64_t N, int64_t K, int group, int q, uint16_t* y,
                             hipStream_t stream) {
-  SSQ_DISPATCH_QGZ(gemv_dispatch, q, group, zp != nullptr, x, codes, scales, zp, N, K, y, stream);
+  SSQ_DISPATCH_QGM(gemv_dispatch, q, group, meta.kind, x, codes, scales, meta.ptr, N, K, y, stream);
 }
 
 hipError_t launch_matmul_f32(const float* x, int64_t M, const uint8_t* codes,
-                             const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
+                             const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K,
                              int group, int q, float* y, hipStream_t stream) {
-  SSQ_DISPATCH_QGZ(f32_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y, stream);
+  SSQ_DISPATCH_QGM(f32_dispatch, q, group, meta.kind, x, M, codes, scales, meta.ptr, N, K, y, stream);
 }
 
 }  // namespace ssq

@@ -1,8 +1,9 @@
 // Weight dequantization for the MFMA kernels (GEMM and skinny-M matmul).
 //
 // App. B.3 of the paper: the weight a code stands for is s*(u - o), with o = 2^(q-1)
-// for the symmetric formats and o = z for the asymmetric one.  These helpers turn a
-// thread's share of a 32-weight block of packed codes into bf16 MFMA operands.
+// for the symmetric formats and o = z for the asymmetric one; the Q*_1 layout of
+// App. B.1 stores a minimum m instead (s*u + m).  These helpers turn a thread's share
+// of a 32-weight block of packed codes into bf16 MFMA operands.
 #pragma once
 
 #include "ssq_internal.h"
@@ -100,6 +101,30 @@ __device__ __forceinline__ void dequant_part(const uint32_t (&d)[Part<Q, P>::kDw
 #pragma unroll
   for (int k = 0; k < kF / 2; ++k) w[k] = pack_bf16x2(f[2 * k], f[2 * k + 1]);
 }
+
+// Constant term `so` of the dequantization (1024 + u)*s + so for each metadata layout:
+// -(1024 + o)*s with the offset o = 2^(q-1) (symmetric) or the zero point z (both
+// products exact: 11-bit by 11-bit), or m - 1024*s for the binary16 minimum layout
+// (one rounding; the weight s*u + m is then within an ulp of fp32).
+template <int META, int Q>
+__device__ __forceinline__ float dequant_offset(float s, uint32_t meta_bits) {
+  if constexpr (META == kMetaMin) {
+    return __builtin_fmaf(-1024.0f, s, f16_bits_to_f32(meta_bits));
+  } else {
+    const float o = META == kMetaZp ? (float)meta_bits : (float)(1 << (Q - 1));
+    return -(1024.0f + o) * s;
+  }
+}
+
+// Load of one group's metadata (zero point u8 or binary16 minimum) at group index gi.
+template <int META>
+__device__ __forceinline__ uint32_t load_group_meta(__amdgpu_buffer_rsrc_t r, uint32_t gi, bool in) {
+  if constexpr (META == kMetaMin) return __builtin_amdgcn_raw_buffer_load_b16(r, in ? gi * 2 : 0x80000000u, 0, 0);
+  else if constexpr (META == kMetaZp) return __builtin_amdgcn_raw_buffer_load_b8(r, in ? gi : 0x80000000u, 0, 0);
+  else return 0u;
+}
+template <int META>
+constexpr int meta_size() { return META == kMetaMin ? 2 : META == kMetaZp ? 1 : 0; }
 
 // s_waitcnt on the vector-memory counter only (gfx9 encoding: vmcnt in bits 3:0 and
 // 15:14, expcnt 6:4 and lgkmcnt 11:8 left at their maxima).  Loads complete in order,

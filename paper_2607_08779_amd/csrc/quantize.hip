@@ -2,7 +2,8 @@
 //
 // Sec. 3 of the paper: Eq. (2) min-max grid, Eq. (3) absmax grid, Eq. (4)-(5)
 // signed absmax grid and its sign rule; Eq. (1) is the quantizer all three use.
-// App. B.1: one binary16 scale per group and packed few-bit indices.
+// App. B.1: one binary16 scale per group and packed few-bit indices (the Q*_1 layout
+// adds a binary16 minimum per group).
 //
 // Mapping.  The matrix is one flat stream of rows*cols weights (cols is a
 // multiple of the group, so no group straddles a row).  Each lane owns a chunk
@@ -68,7 +69,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
                                                             int64_t total_chunks,
                                                             uint8_t* __restrict__ codes,
                                                             uint16_t* __restrict__ scales,
-                                                            uint8_t* __restrict__ zp) {
+                                                            void* __restrict__ meta) {
   constexpr int kLanesPerGroup = G / 8;
   constexpr float kLo = -(float)(1 << (Q - 1));          // min A_q (signed alphabet)
   constexpr float kHi = (float)((1 << (Q - 1)) - 1);     // max A_q
@@ -101,7 +102,8 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
     uint32_t packed = 0;
     uint16_t scale_bits = 0;
     uint8_t zero_point = 0;
-    if constexpr (MODE != 2) {
+    uint16_t min_bits = 0;
+    if constexpr (MODE == 0 || MODE == 1) {
       // Eq. (3) / Eq. (5): M = ||w||_inf, alpha = M / 2^(q-1) (exact), s = gamma*alpha with
       // gamma = -1 iff the largest magnitude is a positive entry not matched by a negative one.
       const float amax = fmaxf(mx, nmn);
@@ -142,15 +144,22 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
       }
       scale_bits = amax == 0.0f ? (uint16_t)0 : f32_to_f16_bits(s);
     } else {
-      // Eq. (2) on the range widened to contain 0, so the integer zero point fits [0, 2^q-1].
-      const float mx0 = fmaxf(mx, 0.0f);
-      const float mn0 = fminf(-nmn, 0.0f);
-      const float s = (mx0 - mn0) / kTop;
+      // Eq. (2).  MODE 2 (u8 zero point): the range widened to contain 0, so the integer
+      // zero point fits [0, 2^q-1].  MODE 3 (binary16 minimum, the Q*_1 layout of
+      // App. B.1): the group's own range, codes rint((w - min)/s) -- Eq. (1) with the
+      // real zero point -min/s -- and the minimum stored beside the scale.
+      const float lo_v = MODE == 2 ? fminf(-nmn, 0.0f) : -nmn;
+      const float hi_v = MODE == 2 ? fmaxf(mx, 0.0f) : mx;
+      const float s = (hi_v - lo_v) / kTop;
+      if constexpr (MODE == 3) {       // a minimum that is (or rounds to) a zero is stored as +0
+        min_bits = f32_to_f16_bits(lo_v);
+        if ((min_bits & 0x7FFFu) == 0) min_bits = 0;
+      }
       if (s != 0.0f) {
-        // rint(fl32(a/s)) without a division, for the zero point (a = -mn0) and every
-        // weight (a = w).  0 lies in [mn0, mx0], so |a| <= mx0 - mn0 and
-        // |a/s| < 2^q - 1 + 2^-16 < 16.  With r = rcp(s) (within 1 ulp of 1/s; s is
-        // normal and far from overflow), t = a*r is within 0.75 * 2^-18 of a/s, and
+        // rint(fl32(a/s)) without a division, for the zero point (a = -min') and every
+        // weight (a = w, or a = fl32(w - min) for MODE 3).  In both cases |a| <= the
+        // range, so |a/s| < 2^q - 1 + 2^-16 < 16.  With r = rcp(s) (within 1 ulp of 1/s;
+        // s is normal and far from overflow), t = a*r is within 0.75 * 2^-18 of a/s, and
         // fl32(a/s) within 2^-21 of a/s, so fl32(a/s) lies within 2^-18 of t.  When t is
         // farther than 2^-18 from every half-integer (|t - rint(t)| < 1/2 - 2^-18, an
         // exact difference), rint(t) is rint(fl32(a/s)).  Otherwise the half-integer h
@@ -169,10 +178,10 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
           }
           return c;
         };
-        const float z = fminf(fmaxf(rint_quotient(-mn0), 0.0f), kTop);
+        const float z = MODE == 2 ? fminf(fmaxf(rint_quotient(-lo_v), 0.0f), kTop) : 0.0f;
         float rq[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) rq[i] = rint_quotient(w[u][i]);
+        for (int i = 0; i < 8; ++i) rq[i] = rint_quotient(MODE == 2 ? w[u][i] : w[u][i] - lo_v);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const float c = fminf(fmaxf(rq[i] + z, 0.0f), kTop);
@@ -186,27 +195,29 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
     store_codes<Q>(codes, chunk, packed, valid);
     if (valid && (chunk % kLanesPerGroup) == 0) {
       scales[chunk / kLanesPerGroup] = scale_bits;
-      if constexpr (MODE == 2) zp[chunk / kLanesPerGroup] = zero_point;
+      if constexpr (MODE == 2) static_cast<uint8_t*>(meta)[chunk / kLanesPerGroup] = zero_point;
+      if constexpr (MODE == 3) static_cast<uint16_t*>(meta)[chunk / kLanesPerGroup] = min_bits;
     }
   }
 }
 
 template <typename In, int Q, int G>
 hipError_t launch_mode(const In* W, int64_t total_chunks, int mode, uint8_t* codes,
-                       uint16_t* scales, uint8_t* zp, hipStream_t stream) {
+                       uint16_t* scales, void* zp, hipStream_t stream) {
   const int64_t per_block = (int64_t)kThreads * kUnroll;
   const dim3 grid((unsigned)((total_chunks + per_block - 1) / per_block));
   switch (mode) {
     case 0: quantize_kernel<In, Q, G, 0><<<grid, kThreads, 0, stream>>>(W, total_chunks, codes, scales, zp); break;
     case 1: quantize_kernel<In, Q, G, 1><<<grid, kThreads, 0, stream>>>(W, total_chunks, codes, scales, zp); break;
-    default: quantize_kernel<In, Q, G, 2><<<grid, kThreads, 0, stream>>>(W, total_chunks, codes, scales, zp); break;
+    case 2: quantize_kernel<In, Q, G, 2><<<grid, kThreads, 0, stream>>>(W, total_chunks, codes, scales, zp); break;
+    default: quantize_kernel<In, Q, G, 3><<<grid, kThreads, 0, stream>>>(W, total_chunks, codes, scales, zp); break;
   }
   return hipGetLastError();
 }
 
 template <typename In, int Q>
 hipError_t launch_group(const In* W, int64_t total_chunks, int group, int mode, uint8_t* codes,
-                        uint16_t* scales, uint8_t* zp, hipStream_t stream) {
+                        uint16_t* scales, void* zp, hipStream_t stream) {
   switch (group) {
     case 32: return launch_mode<In, Q, 32>(W, total_chunks, mode, codes, scales, zp, stream);
     case 64: return launch_mode<In, Q, 64>(W, total_chunks, mode, codes, scales, zp, stream);
@@ -216,7 +227,7 @@ hipError_t launch_group(const In* W, int64_t total_chunks, int group, int mode, 
 
 template <typename In>
 hipError_t launch_any(const In* W, int64_t rows, int64_t cols, int group, int q, int mode,
-                      uint8_t* codes, uint16_t* scales, uint8_t* zp, hipStream_t stream) {
+                      uint8_t* codes, uint16_t* scales, void* zp, hipStream_t stream) {
   const int64_t total_chunks = rows * cols / 8;
   if (total_chunks == 0) return hipSuccess;
   switch (q) {
@@ -229,13 +240,13 @@ hipError_t launch_any(const In* W, int64_t rows, int64_t cols, int group, int q,
 }  // namespace
 
 hipError_t launch_quantize_bf16(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
-                                int mode, uint8_t* codes, uint16_t* scales, uint8_t* zp,
+                                int mode, uint8_t* codes, uint16_t* scales, void* zp,
                                 hipStream_t stream) {
   return launch_any<uint16_t>(W, rows, cols, group, q, mode, codes, scales, zp, stream);
 }
 
 hipError_t launch_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
-                               int mode, uint8_t* codes, uint16_t* scales, uint8_t* zp,
+                               int mode, uint8_t* codes, uint16_t* scales, void* zp,
                                hipStream_t stream) {
   return launch_any<float>(W, rows, cols, group, q, mode, codes, scales, zp, stream);
 }

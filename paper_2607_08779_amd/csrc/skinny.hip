@@ -34,10 +34,10 @@ namespace {
 constexpr int kMaxWaves = 16;
 constexpr uint32_t kOutOfRange = 0x80000000u;   // past every buffer's size: loads return 0
 
-template <int Q, int G, bool ZP, int MB>
+template <int Q, int G, int META, int MB>
 __global__ __launch_bounds__(1024) void skinny_kernel(
     const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zp, int N, int K,
+    const uint16_t* __restrict__ scales, const void* __restrict__ meta, int N, int K,
     uint16_t* __restrict__ y) {
   __shared__ float red[kMaxWaves][MB * 256];   // per wave: its partial D tiles, lane order
 
@@ -53,14 +53,17 @@ __global__ __launch_bounds__(1024) void skinny_kernel(
   const int sb_end = std::min(nsb, sb_begin + per);
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
   const uint32_t groups_per_row = (uint32_t)(K / G);
-  constexpr float kSymOffset = (float)(1 << (Q - 1));
 
   // Descriptors over this workgroup's rows (rows past N read zeros) and over x (tokens
   // past M read zeros; M*K*2 < 2^28 for M <= 32).
   const uint32_t rows = (uint32_t)std::min<int64_t>(16, N - n0);
   const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + n0 * row_bytes, rows * row_bytes);
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + n0 * groups_per_row, rows * groups_per_row * 2);
-  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + n0 * groups_per_row : zp, ZP ? rows * groups_per_row : 0);
+  constexpr bool ZP = META != kMetaNone;
+  constexpr int kMetaSize = meta_size<META>();
+  const uint8_t* const zp = static_cast<const uint8_t*>(meta);
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + n0 * groups_per_row * kMetaSize : zp,
+                                              ZP ? rows * groups_per_row * kMetaSize : 0);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)M * (uint32_t)K * 2);
 
   struct Slot {
@@ -80,7 +83,7 @@ __global__ __launch_bounds__(1024) void skinny_kernel(
     load_part<Q, 1>(rc, in ? (uint32_t)lrow * row_bytes + (uint32_t)blk * (4 * Q) : kOutOfRange, 0, t.d);
     const uint32_t gi = (uint32_t)lrow * groups_per_row + (uint32_t)(blk / (G / 32));
     t.s = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? gi * 2 : kOutOfRange, 0, 0);
-    if constexpr (ZP) t.z = __builtin_amdgcn_raw_buffer_load_b8(rz, in ? gi : kOutOfRange, 0, 0);
+    if constexpr (ZP) t.z = load_group_meta<META>(rz, gi, in);
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       const uint32_t m = (uint32_t)(mb * 16 + lrow);
@@ -128,9 +131,8 @@ __global__ __launch_bounds__(1024) void skinny_kernel(
         t.a[mb][2][e] = p23[0]; t.a[mb][3][e] = p23[1];
       }
     const float s = f16_bits_to_f32(t.s);
-    const float o = ZP ? (float)t.z : kSymOffset;
     uint32_t w[16];
-    dequant_part<Q, 1>(t.d, 0, s, -(1024.0f + o) * s, w);   // exact: 11-bit x 11-bit products
+    dequant_part<Q, 1>(t.d, 0, s, dequant_offset<META, Q>(s, ZP ? t.z : 0u), w);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const bf16x8 b = __builtin_bit_cast(bf16x8, u32x4{w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]});
@@ -210,10 +212,10 @@ SplitPlan split_plan(int64_t M, int64_t N, int64_t K) {
   return p;
 }
 
-template <int Q, int G, bool ZP, int MB>
+template <int Q, int G, int META, int MB>
 __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
     const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales, const uint8_t* __restrict__ zp, int N, int K,
+    const uint16_t* __restrict__ scales, const void* __restrict__ meta, int N, int K,
     uint16_t* __restrict__ y, int splits, int per, float* __restrict__ partials,
     unsigned int* __restrict__ counters) {
   constexpr int kStage = MB * 16 * 128 * 2;    // MB*16 tokens x 128 k, bf16
@@ -230,13 +232,16 @@ __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
   const int nsteps = std::min(nsb, sb_begin + per) - sb_begin;
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
   const uint32_t groups_per_row = (uint32_t)(K / G);
-  constexpr float kSymOffset = (float)(1 << (Q - 1));
 
   const uint32_t rows = (uint32_t)std::max<int64_t>(0, std::min<int64_t>(16, N - n0));
   const int64_t nb = rows ? n0 : 0;
   const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + nb * row_bytes, rows * row_bytes);
   const __amdgpu_buffer_rsrc_t rs = make_rsrc(scales + nb * groups_per_row, rows * groups_per_row * 2);
-  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + nb * groups_per_row : zp, ZP ? rows * groups_per_row : 0);
+  constexpr bool ZP = META != kMetaNone;
+  constexpr int kMetaSize = meta_size<META>();
+  const uint8_t* const zp = static_cast<const uint8_t*>(meta);
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(ZP ? zp + nb * groups_per_row * kMetaSize : zp,
+                                              ZP ? rows * groups_per_row * kMetaSize : 0);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)M * (uint32_t)K * 2);
 
   // Activation chunk of a super-block in LDS (one stage per super-block of the chunk):
@@ -277,7 +282,7 @@ __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
     load_part<Q, 1>(rc, in ? (uint32_t)lrow * row_bytes + (uint32_t)blk * (4 * Q) : kOutOfRange, 0, t.d);
     const uint32_t gi = (uint32_t)lrow * groups_per_row + (uint32_t)(blk / (G / 32));
     t.s = __builtin_amdgcn_raw_buffer_load_b16(rs, in ? gi * 2 : kOutOfRange, 0, 0);
-    if constexpr (ZP) t.z = __builtin_amdgcn_raw_buffer_load_b8(rz, in ? gi : kOutOfRange, 0, 0);
+    if constexpr (ZP) t.z = load_group_meta<META>(rz, gi, in);
   };
   constexpr int kWLoads = 2 + (ZP ? 1 : 0);     // vector loads of issue_w
 
@@ -292,9 +297,8 @@ __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
     t.s = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.s);
     if constexpr (ZP) t.z = (uint32_t)__builtin_amdgcn_ds_bpermute(perm, (int)t.z);
     const float s = f16_bits_to_f32(t.s);
-    const float o = ZP ? (float)t.z : kSymOffset;
     uint32_t w[16];
-    dequant_part<Q, 1>(t.d, 0, s, -(1024.0f + o) * s, w);   // exact: 11-bit x 11-bit products
+    dequant_part<Q, 1>(t.d, 0, s, dequant_offset<META, Q>(s, ZP ? t.z : 0u), w);
     const uint8_t* xb = xs + stage * kStage + am * 256;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -381,9 +385,9 @@ __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
     }
 }
 
-template <int Q, int G, bool ZP>
+template <int Q, int G, int META>
 hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
-                           const uint8_t* zp, int64_t N, int64_t K, uint16_t* y, void* workspace,
+                           const void* zp, int64_t N, int64_t K, uint16_t* y, void* workspace,
                            size_t workspace_bytes, hipStream_t stream) {
   const SplitPlan p = split_plan(M, N, K);
   if (p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace) {
@@ -393,10 +397,10 @@ hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, c
     const int per = (int)((nsb + p.splits - 1) / p.splits);
     const dim3 grid((unsigned)p.row_blocks, (unsigned)p.splits), block(64 * kSplitWaves);
     if (p.mb == 1)
-      skinny_split_kernel<Q, G, ZP, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
+      skinny_split_kernel<Q, G, META, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
                                                                    y, p.splits, per, partials, counters);
     else
-      skinny_split_kernel<Q, G, ZP, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
+      skinny_split_kernel<Q, G, META, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
                                                                    y, p.splits, per, partials, counters);
     return hipGetLastError();
   }
@@ -404,20 +408,20 @@ hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, c
   const int waves = (int)std::min<int64_t>(kMaxWaves, nsb);
   const dim3 grid((unsigned)((N + 15) / 16)), block((unsigned)(64 * waves));
   if (M <= 16)
-    skinny_kernel<Q, G, ZP, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+    skinny_kernel<Q, G, META, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
   else
-    skinny_kernel<Q, G, ZP, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+    skinny_kernel<Q, G, META, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_skinny_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
-                              const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
+                              const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K,
                               int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
                               hipStream_t stream) {
   if (M < 2 || M > kSkinnyMaxM) return hipErrorInvalidValue;
-  SSQ_DISPATCH_QGZ(skinny_dispatch, q, group, zp != nullptr, x, M, codes, scales, zp, N, K, y, workspace,
+  SSQ_DISPATCH_QGM(skinny_dispatch, q, group, meta.kind, x, M, codes, scales, meta.ptr, N, K, y, workspace,
                    workspace_bytes, stream);
 }
 

@@ -48,17 +48,27 @@ int check_matmul(const void* x, int64_t M, const uint8_t* codes, const uint16_t*
   return SSQ_OK;
 }
 
+ssq::GroupMeta zero_points(const uint8_t* zp) { return {zp, zp ? ssq::kMetaZp : ssq::kMetaNone}; }
+ssq::GroupMeta minimums(const uint16_t* mins) { return {mins, ssq::kMetaMin}; }
+
 // bf16 matmul kernel choice by token count: streaming GEMV (M = 1), skinny-M MFMA
 // kernel (batched decode), tiled MFMA GEMM with an optional split reduction (prefill).
 int dispatch_bf16(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
-                  const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                  ssq::GroupMeta meta, int64_t N, int64_t K, int group, int q, uint16_t* y,
                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, zp, N, K, group, q, y, stream));
+  if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, meta, N, K, group, q, y, stream));
   if (M <= ssq::kSkinnyMaxM)
-    return status_of(ssq::launch_skinny_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace,
+    return status_of(ssq::launch_skinny_bf16(x, M, codes, scales, meta, N, K, group, q, y, workspace,
                                              workspace_bytes, stream));
-  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace,
+  return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, meta, N, K, group, q, y, workspace,
                                          workspace_bytes, stream));
+}
+
+// Shared checks of the binary16-minimum entry points: a minimum per group, 2-byte aligned.
+int check_mins(const uint16_t* mins, bool needed) {
+  if (!needed) return SSQ_OK;
+  if (mins == nullptr) return SSQ_EINVAL;
+  return aligned(mins, 2) ? SSQ_OK : SSQ_EALIGN;
 }
 
 }  // namespace
@@ -70,6 +80,24 @@ int ssq_quantize(const uint16_t* W, int64_t rows, int64_t cols, int group, int q
   const int st = check_quantize(W, rows, cols, group, q, mode, codes, scales, zp);
   if (st != SSQ_OK || rows == 0 || cols == 0) return st;
   return status_of(ssq::launch_quantize_bf16(W, rows, cols, group, q, mode, codes, scales, zp, nullptr));
+}
+
+int ssq_quantize_min(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                     uint8_t* codes, uint16_t* scales, uint16_t* mins) {
+  int st = check_quantize(W, rows, cols, group, q, SSQ_SIGNED_SYM, codes, scales, nullptr);
+  if (st == SSQ_OK) st = check_mins(mins, rows > 0 && cols > 0);
+  if (st != SSQ_OK || rows == 0 || cols == 0) return st;
+  return status_of(ssq::launch_quantize_bf16(W, rows, cols, group, q, ssq::kModeAsymMin, codes, scales,
+                                             mins, nullptr));
+}
+
+int ssq_quantize_min_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                         uint8_t* codes, uint16_t* scales, uint16_t* mins) {
+  int st = check_quantize(W, rows, cols, group, q, SSQ_SIGNED_SYM, codes, scales, nullptr);
+  if (st == SSQ_OK) st = check_mins(mins, rows > 0 && cols > 0);
+  if (st != SSQ_OK || rows == 0 || cols == 0) return st;
+  return status_of(ssq::launch_quantize_f32(W, rows, cols, group, q, ssq::kModeAsymMin, codes, scales,
+                                            mins, nullptr));
 }
 
 int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int q, int mode,
@@ -84,7 +112,16 @@ int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_
                hipStream_t stream) {
   const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
   if (st != SSQ_OK || M == 0 || N == 0) return st;
-  return dispatch_bf16(x, M, codes, scales, zp, N, K, group, q, y, nullptr, 0, stream);
+  return dispatch_bf16(x, M, codes, scales, zero_points(zp), N, K, group, q, y, nullptr, 0, stream);
+}
+
+int ssq_matmul_min(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                   const uint16_t* mins, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                   hipStream_t stream) {
+  int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
+  if (st == SSQ_OK) st = check_mins(mins, M > 0 && N > 0);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  return dispatch_bf16(x, M, codes, scales, minimums(mins), N, K, group, q, y, nullptr, 0, stream);
 }
 
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q) {
@@ -98,7 +135,19 @@ int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint
   const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
   if (st != SSQ_OK || M == 0 || N == 0) return st;
   if (workspace != nullptr && !aligned(workspace, 256)) return SSQ_EALIGN;
-  return dispatch_bf16(x, M, codes, scales, zp, N, K, group, q, y, workspace, workspace_bytes, stream);
+  return dispatch_bf16(x, M, codes, scales, zero_points(zp), N, K, group, q, y, workspace, workspace_bytes,
+                       stream);
+}
+
+int ssq_matmul_min_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                      const uint16_t* mins, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
+  if (st == SSQ_OK) st = check_mins(mins, M > 0 && N > 0);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  if (workspace != nullptr && !aligned(workspace, 256)) return SSQ_EALIGN;
+  return dispatch_bf16(x, M, codes, scales, minimums(mins), N, K, group, q, y, workspace, workspace_bytes,
+                       stream);
 }
 
 int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
@@ -106,14 +155,23 @@ int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16
                    hipStream_t stream) {
   const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
   if (st != SSQ_OK || M == 0 || N == 0) return st;
-  return status_of(ssq::launch_matmul_f32(x, M, codes, scales, zp, N, K, group, q, y, stream));
+  return status_of(ssq::launch_matmul_f32(x, M, codes, scales, zero_points(zp), N, K, group, q, y, stream));
+}
+
+int ssq_matmul_min_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                       const uint16_t* mins, int64_t N, int64_t K, int group, int q, float* y,
+                       hipStream_t stream) {
+  int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
+  if (st == SSQ_OK) st = check_mins(mins, M > 0 && N > 0);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  return status_of(ssq::launch_matmul_f32(x, M, codes, scales, minimums(mins), N, K, group, q, y, stream));
 }
 
 const char* ssq_strerror(int status) {
   switch (status) {
     case SSQ_OK: return "success";
-    case SSQ_EINVAL: return "invalid argument (size, q, group, mode or zero-point/mode mismatch)";
-    case SSQ_EALIGN: return "misaligned pointer (W, x, y, codes need 16 bytes; scales 2; workspace 256)";
+    case SSQ_EINVAL: return "invalid argument (size, q, group, mode, zero-point/mode mismatch or missing minimums)";
+    case SSQ_EALIGN: return "misaligned pointer (W, x, y, codes need 16 bytes; scales, mins 2; workspace 256)";
     case SSQ_EHIP: return "HIP runtime error at kernel launch";
     default: return "unknown status";
   }

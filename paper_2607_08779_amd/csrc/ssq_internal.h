@@ -146,42 +146,55 @@ __device__ __forceinline__ float group_sum(float v) {
   return v;
 }
 
-// Instantiate FN<q, group, has_zp>(args...) for the supported (q, group) pairs and
+// Per-group metadata stored beside the scales: none (the symmetric formats), an
+// integer zero point (u8, the weight reads s*(u - z)) or a binary16 minimum (the Q*_1
+// layout of App. B.1, the weight reads s*u + m).
+enum : int { kMetaNone = 0, kMetaZp = 1, kMetaMin = 2 };
+struct GroupMeta {
+  const void* ptr;   // u8 [N, K/group] zero points, u16 [N, K/group] binary16 minimums, or null
+  int kind;          // kMetaNone, kMetaZp or kMetaMin
+};
+
+// Instantiate FN<q, group, meta kind>(args...) for the supported (q, group) pairs and
 // return its result from the enclosing function.
-#define SSQ_DISPATCH_QGZ(FN, q, group, has_zp, ...)                                          \
-  do {                                                                                     \
-    switch (q * 1000 + group * 2 + (has_zp ? 1 : 0)) {                                     \
-      case 2064: return FN<2, 32, false>(__VA_ARGS__);  case 2065: return FN<2, 32, true>(__VA_ARGS__); \
-      case 2128: return FN<2, 64, false>(__VA_ARGS__);  case 2129: return FN<2, 64, true>(__VA_ARGS__); \
-      case 2256: return FN<2, 128, false>(__VA_ARGS__); case 2257: return FN<2, 128, true>(__VA_ARGS__); \
-      case 3064: return FN<3, 32, false>(__VA_ARGS__);  case 3065: return FN<3, 32, true>(__VA_ARGS__); \
-      case 3128: return FN<3, 64, false>(__VA_ARGS__);  case 3129: return FN<3, 64, true>(__VA_ARGS__); \
-      case 3256: return FN<3, 128, false>(__VA_ARGS__); case 3257: return FN<3, 128, true>(__VA_ARGS__); \
-      case 4064: return FN<4, 32, false>(__VA_ARGS__);  case 4065: return FN<4, 32, true>(__VA_ARGS__); \
-      case 4128: return FN<4, 64, false>(__VA_ARGS__);  case 4129: return FN<4, 64, true>(__VA_ARGS__); \
-      case 4256: return FN<4, 128, false>(__VA_ARGS__); case 4257: return FN<4, 128, true>(__VA_ARGS__); \
-      default: return hipErrorInvalidValue;                                                \
-    }                                                                                      \
+#define SSQ_DISPATCH_QGM_CASE(FN, Q, G, ...)                                                   \
+  case Q * 1000 + G * 3 + 0: return FN<Q, G, 0>(__VA_ARGS__);                                \
+  case Q * 1000 + G * 3 + 1: return FN<Q, G, 1>(__VA_ARGS__);                                \
+  case Q * 1000 + G * 3 + 2: return FN<Q, G, 2>(__VA_ARGS__);
+#define SSQ_DISPATCH_QGM(FN, q, group, kind, ...)                                              \
+  do {                                                                                       \
+    switch (q * 1000 + group * 3 + kind) {                                                   \
+      SSQ_DISPATCH_QGM_CASE(FN, 2, 32, __VA_ARGS__) SSQ_DISPATCH_QGM_CASE(FN, 2, 64, __VA_ARGS__)     \
+      SSQ_DISPATCH_QGM_CASE(FN, 2, 128, __VA_ARGS__) SSQ_DISPATCH_QGM_CASE(FN, 3, 32, __VA_ARGS__)    \
+      SSQ_DISPATCH_QGM_CASE(FN, 3, 64, __VA_ARGS__) SSQ_DISPATCH_QGM_CASE(FN, 3, 128, __VA_ARGS__)    \
+      SSQ_DISPATCH_QGM_CASE(FN, 4, 32, __VA_ARGS__) SSQ_DISPATCH_QGM_CASE(FN, 4, 64, __VA_ARGS__)     \
+      SSQ_DISPATCH_QGM_CASE(FN, 4, 128, __VA_ARGS__)                                         \
+      default: return hipErrorInvalidValue;                                                  \
+    }                                                                                        \
   } while (0)
 
 // ---------------------------------------------------------------------------
 // Host-side launchers (arguments already validated by the C ABI layer)
 // ---------------------------------------------------------------------------
 
+// Quantize modes: 0 signed symmetric, 1 unsigned symmetric, 2 min-max with a u8 zero
+// point (`meta` = u8 [rows, cols/group]), 3 min-max with a binary16 minimum (`meta` =
+// u16 [rows, cols/group]); `meta` is null for the symmetric modes.
+constexpr int kModeAsymMin = 3;
 hipError_t launch_quantize_bf16(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
-                                int mode, uint8_t* codes, uint16_t* scales, uint8_t* zp,
+                                int mode, uint8_t* codes, uint16_t* scales, void* meta,
                                 hipStream_t stream);
 hipError_t launch_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
-                               int mode, uint8_t* codes, uint16_t* scales, uint8_t* zp,
+                               int mode, uint8_t* codes, uint16_t* scales, void* meta,
                                hipStream_t stream);
 hipError_t launch_gemv_bf16(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
-                            const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                            GroupMeta meta, int64_t N, int64_t K, int group, int q, uint16_t* y,
                             hipStream_t stream);
 hipError_t launch_matmul_f32(const float* x, int64_t M, const uint8_t* codes,
-                             const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
+                             const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K,
                              int group, int q, float* y, hipStream_t stream);
 hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
-                            const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
+                            const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K,
                             int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
                             hipStream_t stream);
 // Workspace bytes that let the GEMM split its reduction (0 when splitting would not help).
@@ -192,7 +205,7 @@ size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 // MFMA operands; with a workspace the reduction is split across workgroups).
 constexpr int64_t kSkinnyMaxM = 32;
 hipError_t launch_skinny_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
-                              const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K,
+                              const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K,
                               int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
 size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K);

@@ -14,7 +14,8 @@ from typing import Optional, Tuple
 import torch
 
 SIGNED_SYM, UNSIGNED_SYM, ASYM = 0, 1, 2
-MODES = {"signed_sym": SIGNED_SYM, "unsigned_sym": UNSIGNED_SYM, "asym": ASYM}
+ASYM_MIN = 3    # min-max grid in the fp16-minimum layout (the ssq_*_min entry points)
+MODES = {"signed_sym": SIGNED_SYM, "unsigned_sym": UNSIGNED_SYM, "asym": ASYM, "asym_min": ASYM_MIN}
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libssq.so")
 
@@ -40,6 +41,12 @@ _EXPORTS = {
                                      ctypes.c_size_t, ctypes.c_void_p]),
     "ssq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
 }
+_Q_MIN = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p])
+_EXPORTS["ssq_quantize_min"] = _Q_MIN
+_EXPORTS["ssq_quantize_min_f32"] = _Q_MIN
+for _name in ("ssq_matmul_min", "ssq_matmul_min_f32", "ssq_matmul_min_ws"):
+    _EXPORTS[_name] = (ctypes.c_int, list(_EXPORTS[_name.replace("_min", "")][1]))
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -89,7 +96,8 @@ def ssq_quantize(W: torch.Tensor, group: int, q: int, mode: int,
     """Quantize W [rows, cols] (bf16 or fp32, on the GPU) group-wise.
 
     Returns (codes u8 [rows, cols*q/8], scales int16 [rows, cols/group] holding
-    binary16 bit patterns, zp u8 [rows, cols/group] for ASYM else None).
+    binary16 bit patterns, zp u8 [rows, cols/group] for ASYM, the binary16 minimums
+    as int16 [rows, cols/group] for ASYM_MIN, else None).
     Runs on the null stream, like the C entry point.
     """
     if W.dim() != 2 or not W.is_contiguous():
@@ -104,11 +112,16 @@ def ssq_quantize(W: torch.Tensor, group: int, q: int, mode: int,
     if out is None:
         codes = torch.empty((rows, cols * q // 8), dtype=torch.uint8, device=W.device)
         scales = torch.empty((rows, cols // group if group else 0), dtype=torch.int16, device=W.device)
-        zp = (torch.empty((rows, cols // group if group else 0), dtype=torch.uint8, device=W.device)
-              if mode == ASYM else None)
+        meta_dtype = {ASYM: torch.uint8, ASYM_MIN: torch.int16}.get(mode)
+        zp = (torch.empty((rows, cols // group if group else 0), dtype=meta_dtype, device=W.device)
+              if meta_dtype is not None else None)
     else:
         codes, scales, zp = out
-    st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, mode, _ptr(codes), _ptr(scales), _ptr(zp))
+    if mode == ASYM_MIN:
+        fn = fn.replace("ssq_quantize", "ssq_quantize_min")
+        st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(codes), _ptr(scales), _ptr(zp))
+    else:
+        st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, mode, _ptr(codes), _ptr(scales), _ptr(zp))
     _check(fn, st)
     return codes, scales, zp
 
@@ -132,7 +145,9 @@ def ssq_matmul(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
     """y [M, N] = x [M, K] @ dequant(codes, scales, zp)^T on the current stream.
 
     x bf16 gives y bf16 (``ssq_matmul``, or ``ssq_matmul_ws`` when a workspace is
-    given); x fp32 gives y fp32 (``ssq_matmul_f32``).
+    given); x fp32 gives y fp32 (``ssq_matmul_f32``).  A ``zp`` of dtype int16
+    holds binary16 minimums (the ASYM_MIN layout) and selects the ``*_min`` entry
+    points; uint8 is the integer zero point; None the symmetric formats.
     """
     if x.dim() != 2 or not x.is_contiguous() or x.shape[1] != K:
         raise ValueError("x must be a contiguous [M, K] tensor")
@@ -142,14 +157,18 @@ def ssq_matmul(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
         fn = "ssq_matmul_f32"
     else:
         raise TypeError("x must be bfloat16 or float32")
+    if zp is not None and zp.dtype not in (torch.uint8, torch.int16):
+        raise TypeError("zp must be uint8 zero points or int16 binary16 minimums")
+    suffix = "_min" if zp is not None and zp.dtype == torch.int16 else ""
     M = x.shape[0]
     y = torch.empty((M, N), dtype=x.dtype, device=x.device) if out is None else out
     if workspace is not None and fn == "ssq_matmul":
-        fn = "ssq_matmul_ws"
-        st = lib().ssq_matmul_ws(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
-                                 _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
-                                 _stream(x.device))
+        fn = "ssq_matmul" + suffix + "_ws"
+        st = getattr(lib(), fn)(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
+                                _ptr(y), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                _stream(x.device))
     else:
+        fn = fn.replace("ssq_matmul", "ssq_matmul" + suffix)
         st = getattr(lib(), fn)(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
                                 _ptr(y), _stream(x.device))
     _check(fn, st)

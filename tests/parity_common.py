@@ -57,11 +57,18 @@ def assert_quant_equal(gpu, ref: O.Quantized, rows_idx=None, tag=""):
         r, g = np.argwhere(s != ref.scales)[0]
         raise AssertionError(f"{tag}: scales differ first at row {r} group {g}: "
                              f"gpu {s[r, g]:#06x} oracle {ref.scales[r, g]:#06x}")
-    if ref.zp is not None:
+    if ref.zp is not None or ref.mins is not None:
         z = zp.cpu().numpy()
         if rows_idx is not None:
             z = z[rows_idx]
-        assert np.array_equal(z, ref.zp), f"{tag}: zero points differ"
+        if ref.mins is not None:     # binary16 minimums, returned as int16 bit patterns
+            zu = z.view(np.uint16)
+            if not np.array_equal(zu, ref.mins):
+                r, g = np.argwhere(zu != ref.mins)[0]
+                raise AssertionError(f"{tag}: minimums differ first at row {r} group {g}: "
+                                     f"gpu {zu[r, g]:#06x} oracle {ref.mins[r, g]:#06x}")
+        else:
+            assert np.array_equal(z, ref.zp), f"{tag}: zero points differ"
     else:
         assert zp is None
 

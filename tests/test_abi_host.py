@@ -23,8 +23,10 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_matmul_workspace_size",
-                                    "ssq_matmul_ws", "ssq_quantize", "ssq_quantize_f32",
+    assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_matmul_min",
+                                    "ssq_matmul_min_f32", "ssq_matmul_min_ws",
+                                    "ssq_matmul_workspace_size", "ssq_matmul_ws", "ssq_quantize",
+                                    "ssq_quantize_f32", "ssq_quantize_min", "ssq_quantize_min_f32",
                                     "ssq_strerror"]
 
 
@@ -117,3 +119,44 @@ def test_binding_fails_loudly_without_library(monkeypatch):
     monkeypatch.setattr(ssq, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         ssq.lib()
+
+
+# ---------------------------------------------------------------------------
+# The binary16-minimum entry points (App. B.1 Q*_1 layout).
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("args", [
+    dict(q=5), dict(group=16), dict(cols=48), dict(rows=-1),
+    dict(W=None), dict(codes=None), dict(scales=None), dict(mins=None),
+])
+def test_quantize_min_rejects_invalid_arguments(args):
+    a = dict(W=P16, rows=4, cols=64, group=32, q=4, codes=P16, scales=P16, mins=P16)
+    a.update(args)
+    for fn in (ssq.lib().ssq_quantize_min, ssq.lib().ssq_quantize_min_f32):
+        assert fn(a["W"], a["rows"], a["cols"], a["group"], a["q"], a["codes"], a["scales"],
+                  a["mins"]) == EINVAL
+
+
+def test_min_entry_points_reject_misaligned_minimums():
+    odd = ctypes.c_void_p((1 << 20) + 1)
+    assert ssq.lib().ssq_quantize_min(P16, 4, 64, 32, 4, P16, P16, odd) == EALIGN
+    assert ssq.lib().ssq_matmul_min(P16, 2, P16, P16, odd, 8, 64, 32, 4, P16, None) == EALIGN
+    assert ssq.lib().ssq_matmul_min_f32(P16, 2, P16, P16, odd, 8, 64, 32, 4, P16, None) == EALIGN
+    assert ssq.lib().ssq_matmul_min_ws(P16, 2, P16, P16, odd, 8, 64, 32, 4, P16, None, 0, None) == EALIGN
+
+
+@pytest.mark.parametrize("args", [dict(K=48), dict(M=-1), dict(q=8), dict(x=None), dict(mins=None)])
+def test_matmul_min_rejects_invalid_arguments(args):
+    a = dict(x=P16, M=2, codes=P16, scales=P16, mins=P16, N=8, K=64, group=32, q=4, y=P16)
+    a.update(args)
+    for fn in (ssq.lib().ssq_matmul_min, ssq.lib().ssq_matmul_min_f32):
+        assert fn(a["x"], a["M"], a["codes"], a["scales"], a["mins"], a["N"], a["K"], a["group"],
+                  a["q"], a["y"], None) == EINVAL
+    assert ssq.lib().ssq_matmul_min_ws(a["x"], a["M"], a["codes"], a["scales"], a["mins"], a["N"],
+                                       a["K"], a["group"], a["q"], a["y"], None, 0, None) == EINVAL
+
+
+def test_min_entry_points_empty_is_a_noop():
+    assert ssq.lib().ssq_quantize_min(None, 0, 64, 32, 4, None, None, None) == 0
+    assert ssq.lib().ssq_matmul_min(None, 0, None, None, None, 8, 64, 32, 4, None, None) == 0
+    assert ssq.lib().ssq_matmul_min_ws(None, 2, None, None, None, 0, 64, 32, 4, None, None, 0, None) == 0

@@ -17,7 +17,7 @@ from tests.parity_common import (assert_quant_equal, log_metric, rel_l2, sample_
 
 pytestmark = pytest.mark.gpu
 
-MODES = [O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM]
+MODES = [O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM, O.ASYM_MIN]
 TOL_BF16 = 2e-2
 TOL_F32 = 1e-3
 
@@ -41,7 +41,7 @@ def check_matmul(w_host, x_host, group, q, mode, rows_idx=None, bf16_w=True, bf1
     ref_q = O.quantize(widen(w_host[sel], bf16_w), group, q, mode)
     assert_quant_equal((codes, scales, zp), ref_q, None if rows_idx is None else sel, tag=tag)
     xr = widen(x_host, bf16_x)
-    y_ref = O.matmul(xr, ref_q.codes, ref_q.scales, ref_q.zp, len(sel), K, group, q)
+    y_ref = O.matmul(xr, ref_q.codes, ref_q.scales, ref_q.zp, len(sel), K, group, q, mins=ref_q.mins)
     for earlier in ys[:-1]:      # same workspace, same answer every call
         err_rep = rel_l2(y_to_f64(earlier)[:, sel], y_ref)
         assert err_rep <= (TOL_BF16 if bf16_x else TOL_F32), f"{tag}: repeated call rel L2 {err_rep:.3e}"

@@ -14,7 +14,7 @@ from tests.parity_common import (assert_quant_equal, sample_rows, to_device, wei
 
 pytestmark = pytest.mark.gpu
 
-MODES = [O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM]
+MODES = [O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM, O.ASYM_MIN]
 
 
 def run_case(w_host, bf16, group, q, mode, rows_idx=None, tag=""):

@@ -463,7 +463,8 @@ def test_asym_min_grid_properties(q):
         mn, mx = Fr(float(row.min())), Fr(float(row.max()))
         exact_s = (mx - mn) / top
         assert abs(s - exact_s) <= exact_s * Fr(1, 2 ** 22)       # two binary32 roundings
-        assert int(r.mins[n, 0]) == struct.unpack("<H", struct.pack("<e", float(row.min())))[0]
+        mbits = struct.unpack("<H", struct.pack("<e", float(row.min())))[0]
+        assert int(r.mins[n, 0]) == (0 if mbits & 0x7FFF == 0 else mbits)
         u = r.u[n]
         assert u[int(np.argmin(row))] == 0 and u[int(np.argmax(row))] == top
         for k, v in enumerate(row):
@@ -511,7 +512,7 @@ def test_degenerate_groups():
     assert int(r.zp[2, 0]) == 0 and (r.u[2] == 15).all()
     r = O.quantize(w, 32, q, ASYM_MIN)     # constant groups: s = 0, codes 0, m = the constant
     assert (r.scales == 0).all() and (r.u == 0).all()
-    assert [int(b) for b in r.mins[:, 0]] == [0x0000, 0x8000, 0x3600]   # +0, -0, 0.375
+    assert [int(b) for b in r.mins[:, 0]] == [0x0000, 0x0000, 0x3600]   # +0, -0 stored as +0, 0.375
 
 
 def test_scale_storage_matches_python_binary16():
