@@ -217,6 +217,59 @@ def quantize(W: np.ndarray, group: int, q: int, mode: int) -> Quantized:
 
 
 # ---------------------------------------------------------------------------
+# Sec. 4: clipped sets, cardinality margin and realised gain (Def. 1, Lemma 1,
+# Corollary 1, Remark 1).
+# ---------------------------------------------------------------------------
+
+class Diagnostics(NamedTuple):
+    """Result of :func:`sign_diagnostics` (per group, row-major)."""
+
+    margin: np.ndarray     # int16 [rows, cols/group]: m(w) = |C_{-g*}| - |C_{g*}|
+    gain: np.ndarray       # float32 [rows, cols/group]: g(w) = Delta_{-g*} - Delta_{g*}
+    tally: np.ndarray      # int64 [3, 3]: groups by (sign m, sign g), index sign + 1
+
+
+def sign_diagnostics(W: np.ndarray, group: int, q: int) -> Diagnostics:
+    """Remark 1's two statistics for every group of the signed absmax grid.
+
+    gamma* is the sign rule of Eq. (5) (with the tie-break reading), alpha = M/2^(q-1)
+    and T = M (1 - 2^-q).  Def. 1 (Eq. (6)): C_gamma = {i : gamma w_i > T}.  The margin
+    is m(w) = |C_{-gamma*}| - |C_{gamma*}|; by Lemma 1 (Eq. (7)) the realised gain
+    g(w) = ||w - Q_{-gamma*}(w)||^2 - ||w - Q_{gamma*}(w)||^2 equals
+    2 alpha (sum_{C_{-gamma*}} (-gamma* w_i - T) - sum_{C_{gamma*}} (gamma* w_i - T)).
+    Everything is evaluated in binary64, where every term and partial sum is exact for
+    binary32 weights; only the final product 2 alpha * (...) rounds (to binary64), and
+    the stored gain is its binary32 rounding.  The tally counts groups by the signs of
+    the stored margin and gain (index sign + 1 along each axis).
+    """
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    if W.ndim != 2 or group < 1 or W.shape[1] % group:
+        raise ValueError("W must be [rows, cols] with cols a multiple of group")
+    rows, cols = W.shape
+    G = W.reshape(rows, cols // group, group).astype(np.float64)
+    mx, mn = G.max(axis=-1), G.min(axis=-1)
+    M = np.maximum(mx, -mn)                                      # ||w||_inf
+    gamma = np.where(mx > -mn, -1.0, 1.0)                        # Eq. (5), tie -> +1
+    T = M * (1.0 - 2.0 ** -q)                                    # exact in binary64
+    alpha2 = M * 2.0 ** (2 - q)                                  # 2 alpha = 2 M / 2^(q-1)
+    size, excess = {}, {}
+    for g in (1.0, -1.0):
+        inC = g * G > T[..., None]                               # Def. 1, Eq. (6)
+        size[g] = inC.sum(axis=-1)
+        excess[g] = np.where(inC, g * G - T[..., None], 0.0).sum(axis=-1)   # exact sums
+    star = gamma == 1.0
+    c_star = np.where(star, size[1.0], size[-1.0])
+    c_other = np.where(star, size[-1.0], size[1.0])
+    e_star = np.where(star, excess[1.0], excess[-1.0])
+    e_other = np.where(star, excess[-1.0], excess[1.0])
+    margin = (c_other - c_star).astype(np.int16)
+    gain = (alpha2 * (e_other - e_star)).astype(np.float32)      # Lemma 1
+    tally = np.zeros((3, 3), np.int64)
+    np.add.at(tally, (np.sign(margin).astype(np.int64) + 1, np.sign(gain).astype(np.int64) + 1), 1)
+    return Diagnostics(margin=margin, gain=gain, tally=tally)
+
+
+# ---------------------------------------------------------------------------
 # App. B.1: packing q-bit indices, several per byte.
 # ---------------------------------------------------------------------------
 

@@ -572,3 +572,75 @@ def test_matmul_unit_vectors_read_back_dequantized_weights():
         for b in range(K // g):
             i = b * g + int(np.argmax(np.abs(w[n, b * g:(b + 1) * g])))
             assert y[i, n] == float(w[n, i])
+
+
+# ---------------------------------------------------------------------------
+# Sec. 4 diagnostics: clipped sets (Def. 1), margin and realised gain (Remark 1).
+# ---------------------------------------------------------------------------
+
+def test_diagnostics_worked_examples(golden_dir):
+    gold = json.load(open(os.path.join(golden_dir, "worked_example_q2.json")))
+    d = O.sign_diagnostics(np.array([gold["w"]], np.float32), gold["group"], gold["q"])
+    # gamma* = -1: C_{-1} = {}, C_{+1} = {0}; g = E + 2 alpha (w_0 - T) - E = 0.25
+    assert int(d.margin[0, 0]) == 1 and float(d.gain[0, 0]) == 0.25
+    assert d.tally[2, 2] == 1 and d.tally.sum() == 1
+    cx = json.load(open(os.path.join(golden_dir, "corollary1_counterexample_q2.json")))
+    w = np.array([cx["w"]], np.float32)
+    d = O.sign_diagnostics(w, w.shape[1], cx["q"])
+    assert int(d.margin[0, 0]) == len(cx["clipped_other"]) - len(cx["clipped_star"]) == 1
+    assert abs(float(d.gain[0, 0]) - (cx["err2_other"] - cx["err2_star"])) < 1e-6   # -0.21 < 0
+    assert d.tally[2, 0] == 1
+
+
+def _rational_grid(v, scale, lo, hi):
+    """Def. 1 and Eq. (1) in exact arithmetic: (rounded index, clipped?, Q(v))."""
+    r = rne(v / scale)
+    return r, not lo <= r <= hi, scale * min(max(r, lo), hi)
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+def test_diagnostics_match_brute_force(q):
+    """Margin and gain against both signed grids quantized in exact rationals, with the
+    clipped set taken from Def. 1's rounding form, not from the threshold T."""
+    rows = np.concatenate([bf16_groups(120, 32, seed=2100 + q), f32_groups(120, 32, seed=2200 + q),
+                           bf16_groups(60, 16, seed=2300 + q)[:, :16].repeat(2, axis=1)])
+    d = O.sign_diagnostics(rows, 32, q)
+    lo, hi = -(1 << (q - 1)), (1 << (q - 1)) - 1
+    n_checked = 0
+    for n, row in enumerate(rows):
+        g = [Fr(float(v)) for v in row]
+        M = max(abs(v) for v in g)
+        if M == 0:
+            assert int(d.margin[n, 0]) == 0 and float(d.gain[n, 0]) == 0.0
+            continue
+        alpha = M / 2 ** (q - 1)
+        if any(near_half(v / alpha, Fr(1, 2 ** 20)) or (v / alpha).denominator == 2 for v in g):
+            continue     # Def. 1 assumes no quotient on a half-integer
+        pos_max = max(g) == M and -min(g) != M      # dominant outlier positive and unmatched
+        gamma_star = -1 if pos_max else 1
+        size, err = {}, {}
+        for gamma in (1, -1):
+            res = [_rational_grid(v, gamma * alpha, lo, hi) for v in g]
+            size[gamma] = sum(1 for _, clipped, _ in res if clipped)
+            err[gamma] = sum((v - qv) ** 2 for v, (_, _, qv) in zip(g, res))
+        m = size[-gamma_star] - size[gamma_star]
+        gain = err[-gamma_star] - err[gamma_star]
+        assert int(d.margin[n, 0]) == m
+        got = Fr(float(d.gain[n, 0]))
+        assert (got > 0) == (gain > 0) and (got < 0) == (gain < 0)
+        assert abs(got - gain) <= abs(gain) * Fr(1, 2 ** 22)
+        n_checked += 1
+    assert n_checked > 200
+
+
+def test_diagnostics_tally_counts_groups():
+    w = np.concatenate([bf16_groups(400, 32, seed=31), f32_groups(100, 32, seed=32),
+                        np.zeros((4, 32), np.float32)])
+    for q in (2, 3, 4):
+        d = O.sign_diagnostics(w, 32, q)
+        assert d.tally.sum() == w.shape[0]
+        for sm in (-1, 0, 1):
+            for sg in (-1, 0, 1):
+                n = int(((np.sign(d.margin) == sm) & (np.sign(d.gain) == sg)).sum())
+                assert d.tally[sm + 1, sg + 1] == n
+        assert d.tally[1, 1] >= 4     # all-zero groups: no clipping either way
