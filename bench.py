@@ -23,8 +23,9 @@ TFLOP/s and the quantize kernel's bandwidth are reported beside it.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
        python bench.py --sweep      (format sweep: all Llama3-8B projections at every
-                                     q, g and mode; the prefill GEMM per mode; the
-                                     Llama3-70B block at q=2 -- one JSON line)
+                                     q, g and mode; the sign-rule diagnostics of that
+                                     block; the prefill GEMM per mode; the Llama3-70B
+                                     block at q=2 -- one JSON line; --sweep-parts picks)
 """
 from __future__ import annotations
 
@@ -93,6 +94,9 @@ def parse_args():
     p.add_argument("--batched-m", type=int, default=16, help="tokens of the batched-decode phase")
     p.add_argument("--sweep", action="store_true",
                    help="format sweep over the Llama3 shapes instead of the headline step")
+    p.add_argument("--sweep-parts", default="formats,diagnostics,prefill,70b",
+                   help="comma list of sweep parts: formats (8B block, every format), diagnostics "
+                        "(sign-rule statistics of the 8B block), prefill, 70b")
     p.add_argument("--phases", default="quantize,gemv,batched,gemm",
                    help="comma list of phases to run (profiling runs isolate one kernel); "
                         "'copy' adds a plain 256 MiB device copy used to calibrate byte counters")
@@ -198,6 +202,12 @@ def quantize_bytes(N, K, q, g, meta):
     return 2 * N * K + N * K * q // 8 + (2 + meta) * N * K // g
 
 
+def diagnostics_bytes(N, K, g):
+    """bf16 weights read, int16 margin and fp32 gain written per group (the tally's
+    per-block counts are a few KB)."""
+    return 2 * N * K + 6 * N * K // g
+
+
 def sweep(args) -> int:
     """Throughput of every format on the Llama3 shapes (event-timed; weights past the
     Infinity Cache for the decode passes).  One JSON line with a row per case."""
@@ -256,14 +266,37 @@ def sweep(args) -> int:
     wl = synth.llama3_8b_block()
     names = list(synth.LLAMA3_8B)
     W = {n: dev_bf16(synth.weights(wl.layers[n])) for n in names}
-    for q in (2, 3, 4):
+    parts = set(args.sweep_parts.split(","))
+    for q in (2, 3, 4) if "formats" in parts else ():
         for g in (32, 64, 128):
             for mode_name in SWEEP_MODES:
                 block_pass(wl, names, q, g, mode_name, (1,))
 
+    # Sign-rule diagnostics (Sec. 4 Remark 1) over the block: per-group margin and gain,
+    # then the tally.  Fig. 1's two statistics are reported from the tally: the share of
+    # groups with m >= 0 (Corollary 1's condition) and the share with g > 0 among those
+    # with m > 0.  Synthetic weights: these are not the paper's model figures.
+    for q in (2, 3, 4) if "diagnostics" in parts else ():
+        for g in (32, 64, 128):
+            outs = {n: (torch.empty((N, K // g), dtype=torch.int16, device=dev),
+                        torch.empty((N, K // g), dtype=torch.float32, device=dev),
+                        torch.empty(9, dtype=torch.int64, device=dev))
+                    for n, (N, K) in ((n, (wl.layers[n].rows, wl.layers[n].cols)) for n in names)}
+            t = _eager_time(torch, lambda: [ssq.ssq_sign_diagnostics(W[n], g, q, out=outs[n]) for n in names], 5)
+            tally = sum(outs[n][2].cpu().view(3, 3) for n in names).numpy()
+            groups = int(tally.sum())
+            db = sum(diagnostics_bytes(wl.layers[n].rows, wl.layers[n].cols, g) for n in names)
+            rows.append({"block": wl.name, "op": "sign_diagnostics", "q": q, "group": g,
+                         "launches": len(names), "us": round(t * 1e6, 2), "bytes": db,
+                         "gbs": round(db / t / 1e9, 1), "frac_hbm": round(db / t / 1e9 / HBM_PEAK_GBS, 4),
+                         "groups": groups, "tally": tally.tolist(),
+                         "frac_margin_ge_0": round(float(tally[1:].sum()) / groups, 4),
+                         "frac_gain_gt_0_given_margin_gt_0": round(float(tally[2, 2]) / max(1, tally[2].sum()), 4)})
+            del outs
+
     # Prefill GEMM (W4 g32) on both MLP orientations, per mode.
     pf = synth.prefill()
-    for n, spec in pf.layers.items():
+    for n, spec in pf.layers.items() if "prefill" in parts else ():
         Wp = dev_bf16(synth.weights(spec))
         N, K = spec.rows, spec.cols
         for mode_name in SWEEP_MODES:
@@ -284,13 +317,14 @@ def sweep(args) -> int:
     torch.cuda.empty_cache()
 
     # Llama3-70B block at q=2, g=32: quantize, then M=1 and M=16 per mode.
-    wl = synth.llama3_70b_block()
-    names = list(synth.LLAMA3_70B)
-    W = {n: dev_bf16(synth.weights(wl.layers[n])) for n in names}
-    for mode_name in SWEEP_MODES:
-        block_pass(wl, names, 2, 32, mode_name, (1, 16))
-    del W
-    torch.cuda.empty_cache()
+    if "70b" in parts:
+        wl = synth.llama3_70b_block()
+        names = list(synth.LLAMA3_70B)
+        W = {n: dev_bf16(synth.weights(wl.layers[n])) for n in names}
+        for mode_name in SWEEP_MODES:
+            block_pass(wl, names, 2, 32, mode_name, (1, 16))
+        del W
+        torch.cuda.empty_cache()
 
     print(json.dumps({"sweep": "format sweep on synthetic Llama3 shapes", "data": "synthetic",
                       "hbm_peak_gbs": HBM_PEAK_GBS, "bf16_peak_tflops": BF16_PEAK_TFLOPS,

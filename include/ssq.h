@@ -205,6 +205,40 @@ int ssq_matmul_min_f32(const float* x, int64_t M, const uint8_t* codes, const ui
                        const uint16_t* mins, int64_t N, int64_t K, int group, int q, float* y,
                        hipStream_t stream);
 
+/*
+ * ssq_sign_diagnostics -- the statistics of Sec. 4 Remark 1 (Fig. 1) for every
+ * group of the signed absmax grid: with gamma* the sign rule of Eq. (5) (ties
+ * +1), alpha = M / 2^(q-1), T = M (1 - 2^-q) and the clipped sets of Def. 1,
+ * C_gamma = {i : gamma w_i > T} (Eq. (6)):
+ *   margin[g] = |C_{-gamma*}| - |C_{gamma*}|            (the cardinality margin m(w))
+ *   gain[g]   = ||w - Q_{-gamma*}(w)||^2 - ||w - Q_{gamma*}(w)||^2
+ *             = 2 alpha (sum_{C_{-gamma*}} (-gamma* w_i - T) - sum_{C_{gamma*}} (gamma* w_i - T))
+ *                                                       (the realised gain g(w), Lemma 1)
+ * Margin is exact; the gain's terms and sums are exact (integer multiples of a
+ * power of two) and only the final product rounds, to binary64 and then to the
+ * stored binary32 (an exact zero gain may be stored as +0 or -0).  m >= 0 is
+ * Corollary 1's condition for gamma* minimising the worst-case bound; g > 0 means
+ * gamma* also lowers the realised l2 error.
+ *
+ *   W      device, bf16 bits [rows, cols] row-major, read only (16-byte aligned)
+ *   rows, cols, group, q   as ssq_quantize
+ *   margin device, int16 [rows, cols/group], written (2-byte aligned)
+ *   gain   device, float [rows, cols/group], written (4-byte aligned)
+ *   tally  device, uint64 [9] or NULL: counts of groups by the signs of the stored
+ *          margin and gain, tally[(sign(m) + 1) * 3 + (sign(g) + 1)]; overwritten,
+ *          all zero when rows or cols is 0 (8-byte aligned)
+ * Weights must be finite.  Enqueued on the null stream, so calls on one device run
+ * one after another: the tally's per-block counts and arrival counter live in a
+ * static device array that consecutive calls reuse.  Returns SSQ_OK or a negative
+ * ssq_status (SSQ_EINVAL also past about 2^38 weights).
+ */
+int ssq_sign_diagnostics(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                         int16_t* margin, float* gain, uint64_t* tally);
+
+/* ssq_sign_diagnostics for binary32 weights W[rows, cols]; otherwise identical. */
+int ssq_sign_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                             int16_t* margin, float* gain, uint64_t* tally);
+
 /* Static description of a status code; never NULL. */
 const char* ssq_strerror(int status);
 

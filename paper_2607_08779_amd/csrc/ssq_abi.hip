@@ -17,14 +17,19 @@ bool valid_q(int q) { return q == 2 || q == 3 || q == 4; }
 bool valid_group(int g) { return g == 32 || g == 64 || g == 128; }
 int status_of(hipError_t e) { return e == hipSuccess ? SSQ_OK : SSQ_EHIP; }
 
-int check_quantize(const void* W, int64_t rows, int64_t cols, int group, int q, int mode,
-                   const uint8_t* codes, const uint16_t* scales, const uint8_t* zp) {
+int check_grid_sizes(int64_t rows, int64_t cols, int group, int q) {
   if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim) return SSQ_EINVAL;
   if (!valid_q(q) || !valid_group(group)) return SSQ_EINVAL;
-  if (mode != SSQ_SIGNED_SYM && mode != SSQ_UNSIGNED_SYM && mode != SSQ_ASYM) return SSQ_EINVAL;
   if (cols % group != 0) return SSQ_EINVAL;
-  if ((mode == SSQ_ASYM) != (zp != nullptr)) return SSQ_EINVAL;
   if (rows * cols > kMaxElems) return SSQ_EINVAL;
+  return SSQ_OK;
+}
+
+int check_quantize(const void* W, int64_t rows, int64_t cols, int group, int q, int mode,
+                   const uint8_t* codes, const uint16_t* scales, const uint8_t* zp) {
+  if (check_grid_sizes(rows, cols, group, q) != SSQ_OK) return SSQ_EINVAL;
+  if (mode != SSQ_SIGNED_SYM && mode != SSQ_UNSIGNED_SYM && mode != SSQ_ASYM) return SSQ_EINVAL;
+  if ((mode == SSQ_ASYM) != (zp != nullptr)) return SSQ_EINVAL;
   if (rows == 0 || cols == 0) return SSQ_OK;
   if (W == nullptr || codes == nullptr || scales == nullptr) return SSQ_EINVAL;
   if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 2)) return SSQ_EALIGN;
@@ -45,6 +50,15 @@ int check_matmul(const void* x, int64_t M, const uint8_t* codes, const uint16_t*
   if (x == nullptr || codes == nullptr || scales == nullptr || y == nullptr) return SSQ_EINVAL;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(y, 16) || !aligned(scales, 2))
     return SSQ_EALIGN;
+  return SSQ_OK;
+}
+
+int check_diagnostics(const void* W, int64_t rows, int64_t cols, int group, int q,
+                      const int16_t* margin, const float* gain, const uint64_t* tally) {
+  if (check_grid_sizes(rows, cols, group, q) != SSQ_OK) return SSQ_EINVAL;
+  if (rows == 0 || cols == 0) return aligned(tally, 8) ? SSQ_OK : SSQ_EALIGN;   // tally only
+  if (W == nullptr || margin == nullptr || gain == nullptr) return SSQ_EINVAL;
+  if (!aligned(W, 16) || !aligned(margin, 2) || !aligned(gain, 4) || !aligned(tally, 8)) return SSQ_EALIGN;
   return SSQ_OK;
 }
 
@@ -165,6 +179,20 @@ int ssq_matmul_min_f32(const float* x, int64_t M, const uint8_t* codes, const ui
   if (st == SSQ_OK) st = check_mins(mins, M > 0 && N > 0);
   if (st != SSQ_OK || M == 0 || N == 0) return st;
   return status_of(ssq::launch_matmul_f32(x, M, codes, scales, minimums(mins), N, K, group, q, y, stream));
+}
+
+int ssq_sign_diagnostics(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                         int16_t* margin, float* gain, uint64_t* tally) {
+  const int st = check_diagnostics(W, rows, cols, group, q, margin, gain, tally);
+  if (st != SSQ_OK || ((rows == 0 || cols == 0) && tally == nullptr)) return st;
+  return status_of(ssq::launch_diagnostics_bf16(W, rows, cols, group, q, margin, gain, tally));
+}
+
+int ssq_sign_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                             int16_t* margin, float* gain, uint64_t* tally) {
+  const int st = check_diagnostics(W, rows, cols, group, q, margin, gain, tally);
+  if (st != SSQ_OK || ((rows == 0 || cols == 0) && tally == nullptr)) return st;
+  return status_of(ssq::launch_diagnostics_f32(W, rows, cols, group, q, margin, gain, tally));
 }
 
 const char* ssq_strerror(int status) {

@@ -210,4 +210,10 @@ hipError_t launch_skinny_bf16(const uint16_t* x, int64_t M, const uint8_t* codes
                               hipStream_t stream);
 size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
+// Sign-rule diagnostics (Sec. 4): per-group margin and gain, optional 3x3 tally.
+hipError_t launch_diagnostics_bf16(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                                   int16_t* margin, float* gain, uint64_t* tally);
+hipError_t launch_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                                  int16_t* margin, float* gain, uint64_t* tally);
+
 }  // namespace ssq

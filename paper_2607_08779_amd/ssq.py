@@ -47,6 +47,8 @@ _EXPORTS["ssq_quantize_min"] = _Q_MIN
 _EXPORTS["ssq_quantize_min_f32"] = _Q_MIN
 for _name in ("ssq_matmul_min", "ssq_matmul_min_f32", "ssq_matmul_min_ws"):
     _EXPORTS[_name] = (ctypes.c_int, list(_EXPORTS[_name.replace("_min", "")][1]))
+_EXPORTS["ssq_sign_diagnostics"] = _Q_MIN
+_EXPORTS["ssq_sign_diagnostics_f32"] = _Q_MIN
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -79,7 +81,12 @@ def ssq_strerror(status: int) -> str:
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
-    return None if t is None else t.data_ptr()
+    """Device address of a GPU tensor; a host tensor would hand a kernel a host pointer."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("ssq kernels take GPU tensors only (got a tensor on %s)" % t.device)
+    return t.data_ptr()
 
 
 def _stream(device: torch.device) -> int:
@@ -173,3 +180,37 @@ def ssq_matmul(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
                                 _ptr(y), _stream(x.device))
     _check(fn, st)
     return y
+
+
+def ssq_sign_diagnostics(W: torch.Tensor, group: int, q: int, tally: bool = True, out=None):
+    """Sec. 4 Remark 1 statistics of the signed absmax grid for every group of W.
+
+    Returns (margin int16 [rows, cols/group] = |C_{-g*}| - |C_{g*}|, gain float32
+    [rows, cols/group] = realised l2 gain of gamma* over -gamma*, tally int64 [3, 3]
+    of groups by (sign margin, sign gain) or None).  `out` = (margin, gain, tally[9] or
+    None) reuses buffers.  Runs on the null stream.
+    """
+    if W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be a contiguous 2-D tensor")
+    if W.dtype == torch.bfloat16:
+        fn = "ssq_sign_diagnostics"
+    elif W.dtype == torch.float32:
+        fn = "ssq_sign_diagnostics_f32"
+    else:
+        raise TypeError("W must be bfloat16 or float32")
+    rows, cols = W.shape
+    shape = (rows, cols // group if group else 0)
+    if out is not None:
+        margin, gain, t = out
+        if (margin.dtype != torch.int16 or gain.dtype != torch.float32 or tuple(margin.shape) != shape
+                or tuple(gain.shape) != shape or not (margin.is_contiguous() and gain.is_contiguous())
+                or (t is not None and (t.dtype != torch.int64 or t.numel() != 9))):
+            raise ValueError("out must be (int16 margin, float32 gain) of shape rows x cols/group "
+                             "and an int64 tally of 9 elements or None")
+    else:
+        margin = torch.empty(shape, dtype=torch.int16, device=W.device)
+        gain = torch.empty(shape, dtype=torch.float32, device=W.device)
+        t = torch.empty(9, dtype=torch.int64, device=W.device) if tally else None
+    st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(margin), _ptr(gain), _ptr(t))
+    _check(fn, st)
+    return margin, gain, (t.view(3, 3) if t is not None else None)

@@ -27,6 +27,7 @@ def test_header_declares_the_boundary():
                                     "ssq_matmul_min_f32", "ssq_matmul_min_ws",
                                     "ssq_matmul_workspace_size", "ssq_matmul_ws", "ssq_quantize",
                                     "ssq_quantize_f32", "ssq_quantize_min", "ssq_quantize_min_f32",
+                                    "ssq_sign_diagnostics", "ssq_sign_diagnostics_f32",
                                     "ssq_strerror"]
 
 
@@ -160,3 +161,32 @@ def test_min_entry_points_empty_is_a_noop():
     assert ssq.lib().ssq_quantize_min(None, 0, 64, 32, 4, None, None, None) == 0
     assert ssq.lib().ssq_matmul_min(None, 0, None, None, None, 8, 64, 32, 4, None, None) == 0
     assert ssq.lib().ssq_matmul_min_ws(None, 2, None, None, None, 0, 64, 32, 4, None, None, 0, None) == 0
+
+
+@pytest.mark.parametrize("args", [
+    dict(q=5), dict(group=16), dict(cols=48), dict(rows=-1),
+    dict(W=None), dict(margin=None), dict(gain=None),
+])
+def test_sign_diagnostics_rejects_invalid_arguments(args):
+    a = dict(W=P16, rows=4, cols=64, group=32, q=4, margin=P16, gain=P16, tally=P16)
+    a.update(args)
+    for fn in (ssq.lib().ssq_sign_diagnostics, ssq.lib().ssq_sign_diagnostics_f32):
+        assert fn(a["W"], a["rows"], a["cols"], a["group"], a["q"], a["margin"], a["gain"],
+                  a["tally"]) == EINVAL
+
+
+def test_sign_diagnostics_alignment_and_empty():
+    lib = ssq.lib()
+    assert lib.ssq_sign_diagnostics(P16, 4, 64, 32, 4, P2, ctypes.c_void_p((1 << 20) + 2), None) == EALIGN
+    assert lib.ssq_sign_diagnostics(P16, 4, 64, 32, 4, P16, P16, ctypes.c_void_p((1 << 20) + 4)) == EALIGN
+    assert lib.ssq_sign_diagnostics(None, 0, 64, 32, 4, None, None, None) == 0
+
+
+def test_binding_refuses_host_tensors():
+    """A CPU tensor never reaches a kernel: the binding raises before any launch."""
+    import torch
+    W = torch.zeros((4, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU tensors"):
+        ssq.ssq_quantize(W, 32, 4, ssq.SIGNED_SYM)
+    with pytest.raises(ValueError, match="GPU tensors"):
+        ssq.ssq_sign_diagnostics(W, 32, 4)

@@ -1,0 +1,99 @@
+"""GPU parity: ssq_sign_diagnostics against the CPU oracle (Sec. 4 Def. 1, Lemma 1,
+Remark 1).  Margins, gains (binary32 values) and the tally must be identical:
+both sides form the gain from exact binary64 sums with one final rounding."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import ssq_oracle as O
+from paper_2607_08779_amd import ssq, synth
+from tests.parity_common import sample_rows, to_device, widen
+
+pytestmark = pytest.mark.gpu
+
+
+def check(w_host, bf16, group, q, rows_idx=None, tag=""):
+    W = to_device(w_host, bf16)
+    margin, gain, tally = ssq.ssq_sign_diagnostics(W, group, q)
+    torch.cuda.synchronize()
+    sel = slice(None) if rows_idx is None else rows_idx
+    with np.errstate(over="ignore"):                     # a gain past binary32 rounds to inf
+        ref = O.sign_diagnostics(widen(w_host[sel], bf16), group, q)
+    m = margin.cpu().numpy()[sel]
+    g = gain.cpu().numpy()[sel]
+    assert np.array_equal(m, ref.margin), f"{tag}: margins differ"
+    # Identical binary32 values; a zero gain is exact and the sign of that zero is an
+    # artifact of which maximum the two sides pick for M when +0 meets -0.
+    if not np.array_equal(g, ref.gain):
+        r, b = np.argwhere(g != ref.gain)[0]
+        raise AssertionError(f"{tag}: gains differ at ({r}, {b}): gpu {g[r, b]!r} oracle {ref.gain[r, b]!r}")
+    if rows_idx is None:
+        assert np.array_equal(tally.cpu().numpy(), ref.tally), f"{tag}: tallies differ"
+    return tally.cpu().numpy()
+
+
+def random_bf16(rows, cols, seed, outliers=0.001):
+    return synth.weights(synth.WeightSpec(rows, cols, nu=5.0, scale=0.02, outlier_frac=outliers, seed=seed))
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+def test_diagnostics_bf16_all_formats(q, group):
+    check(random_bf16(45, 1536, seed=q * 100 + group, outliers=0.01), True, group, q, tag=f"bf16 q={q} g={group}")
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+def test_diagnostics_fp32(q):
+    rng = np.random.default_rng(q)
+    w = (rng.standard_t(4, size=(33, 1024)) * 0.02).astype(np.float32)
+    check(w, False, 32, q, tag=f"f32 q={q}")
+
+
+def test_diagnostics_edge_groups():
+    rng = np.random.default_rng(9)
+    rows = [np.zeros(64, np.float32), -np.zeros(64, np.float32)]
+    t = rng.standard_normal(64).astype(np.float32) * 0.1
+    t[::32] = 1.0; t[1::32] = -1.0                       # +M / -M ties
+    rows.append(t)
+    c = np.zeros(64, np.float32); c[:8] = [1.0, 0.76, 0.76, -0.99, -0.99, 0, 0, 0]   # Corollary 1 counterexample
+    rows.append(c)
+    rows.append(np.full(64, 0.375, np.float32))          # constant groups: everything clipped one way
+    rows.append((rng.standard_normal(64) * 1e-39).astype(np.float32))   # bf16 subnormals
+    rows.append((rng.standard_normal(64) * 1e17).astype(np.float32))
+    rows.append((rng.standard_normal(64) * 1e35).astype(np.float32))   # gains overflow to inf
+    w = synth.to_bf16_bits(np.stack(rows))
+    for q in (2, 3, 4):
+        check(w, True, 32, q, tag=f"edge q={q}")
+
+
+def test_diagnostics_llama3_8b_down_proj_full_size():
+    """4096x14336 at q in {2,3,4}: sampled rows bit for bit; tally consistent with the
+    full per-group outputs (the GPU tally counts what the GPU stored)."""
+    spec = synth.llama3_8b_decode().layers["down_proj"]
+    w = synth.weights(spec)
+    rows = sample_rows(spec.rows, 64, seed=3)
+    for q in (2, 3, 4):
+        tally = check(w, True, 32, q, rows_idx=rows, tag=f"down_proj q={q}")
+        assert tally.sum() == spec.rows * spec.cols // 32
+
+
+def test_diagnostics_tally_across_calls():
+    """The blocks' counts and the arrival counter are reused from call to call: a full
+    grid, a call without a tally, then a small grid must each give the oracle's tally."""
+    big = random_bf16(2048, 4096, seed=11)               # 2^20 chunks: every block of the grid
+    small = random_bf16(6, 256, seed=12)                 # a single block
+    for w, tag in ((big, "big"), (small, "small"), (big, "big again")):
+        W = to_device(w, True)
+        ssq.ssq_sign_diagnostics(W, 32, 2, tally=False)
+        _, _, tally = ssq.ssq_sign_diagnostics(W, 32, 2)
+        torch.cuda.synchronize()
+        ref = O.sign_diagnostics(widen(w, True), 32, 2)
+        assert np.array_equal(tally.cpu().numpy(), ref.tally), tag
+
+
+def test_diagnostics_empty():
+    W = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    margin, gain, tally = ssq.ssq_sign_diagnostics(W, 32, 4)
+    torch.cuda.synchronize()
+    assert margin.shape == (0, 2) and gain.shape == (0, 2)
+    assert tally.cpu().numpy().sum() == 0
