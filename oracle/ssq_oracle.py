@@ -20,6 +20,9 @@ The oracle is written to be read against the paper (Colbert, Dash et al.,
 * App. B.1 (Q4_1 / Q2_1 rows of the formats table): the min-max grid stored as an
   fp16 scale s and an fp16 minimum m per block, so that a weight reads back as
   s*u + m (the real zero point z = -min/s of Eq. (2) folded into m = -s*z).
+* Sec. 5.2 and App. C (dynamic Q8_0 activations, narrow range A = {-127, ..., 127})
+  with App. B.3's integer GEMM term and row-sum correction: ``quantize_act_q8`` and
+  ``matmul_q8``.
 
 Arithmetic precision.  The paper fixes no precision for the grid computation;
 this oracle computes the scale and the quotient w/s in IEEE binary32 (each
@@ -70,6 +73,16 @@ READINGS = {
                 "as s*u + m with the stored binary16 s and m.  A constant group (max == min) "
                 "stores s = 0, codes 0 and m = binary16(min).",
     "index_encoding": "Symmetric codes c in A_q are stored as the offset-binary index u = c + 2^(q-1).",
+    "q8_activations": "Dynamic Q8_0 (per token, blocks of 32, the narrow-range alphabet "
+                      "{-127..127}): d = fl32(amax/127), codes clip(rne(fl32(x/d)), -127, 127) from "
+                      "the binary32 d, stored scale binary16(d) (half to even; it may underflow to "
+                      "0 or overflow to inf, as the format does); an all-zero block stores d = +0 "
+                      "and codes 0.  Input activations are bf16.",
+    "q8_matmul": "App. B.3 with Q8_0 activations: per 32-activation block b inside weight group "
+                 "g, I = sum_j q_j u_j and R = sum_j q_j are exact integers; y = sum_b d_b s_g "
+                 "(I - o_g R) (symmetric offset or zero point o) or sum_b d_b (s_g I + m_g R) "
+                 "(fp16 minimum), each block term exact in binary64 and the sum over blocks in "
+                 "binary64.",
     "bit_order": "Field k of a row occupies bits [k*q, k*q+q) of the row's little-endian bit stream.",
 }
 
@@ -333,3 +346,77 @@ def matmul(x: np.ndarray, codes: np.ndarray, scales: np.ndarray, zp: Optional[np
     if W_hat.shape[0] != N:
         raise ValueError("codes do not have N rows")
     return x64 @ W_hat.T
+
+
+# ---------------------------------------------------------------------------
+# Q8_0 activations and the integer-dot matmul (Sec. 5.2, App. C; App. B.3).
+# ---------------------------------------------------------------------------
+
+Q8_BLOCK = 32       # activations per Q8_0 block (the GGUF block the weight groups align to)
+Q8_MAX = 127        # narrow range: K = 2^(8-1) - 1
+
+
+class QuantizedAct(NamedTuple):
+    q: np.ndarray       # int8 [M, K]: codes in {-127, ..., 127}
+    d: np.ndarray       # uint16 [M, K/32]: binary16 bits of the block scales
+
+
+def quantize_act_q8(x: np.ndarray) -> QuantizedAct:
+    """Dynamic Q8_0 quantization of activations x [M, K] (bf16 values as binary32).
+
+    Per token and block of 32 the narrow-range symmetric grid of App. C: with
+    amax = max |x_j|, d = amax / 127 and q_j = clip(round(x_j / d), -127, 127), i.e.
+    Eq. (1) with z = 0 on A = {-127, ..., 127}.  Readings ``q8_activations``: binary32
+    d and quotient, half to even, stored scale binary16(d); an all-zero block stores
+    d = +0 and codes 0.
+    """
+    X = np.ascontiguousarray(x, dtype=np.float32)
+    if X.ndim != 2 or X.shape[1] % Q8_BLOCK:
+        raise ValueError("x must be [M, K] with K a multiple of 32")
+    M, K = X.shape
+    B = X.reshape(M, K // Q8_BLOCK, Q8_BLOCK)
+    amax = np.abs(B).max(axis=-1)                                   # exact
+    d32 = (amax / np.float32(Q8_MAX)).astype(np.float32)            # one binary32 division
+    zero = amax == 0
+    safe = np.where(zero, np.float32(1), d32)
+    t = (B / safe[..., None]).astype(np.float32)                    # binary32 quotients
+    qv = np.clip(np.rint(t), -Q8_MAX, Q8_MAX)                       # half to even
+    qv = np.where(zero[..., None], 0.0, qv)
+    d16 = f16_bits_from_f32(np.where(zero, np.float32(0), d32))
+    return QuantizedAct(q=qv.astype(np.int8).reshape(M, K), d=d16)
+
+
+def matmul_q8(qx: np.ndarray, dx: np.ndarray, codes: np.ndarray, scales: np.ndarray,
+              zp: Optional[np.ndarray], N: int, K: int, group: int, q: int,
+              mins: Optional[np.ndarray] = None) -> np.ndarray:
+    """y[m, n] for Q8_0 activations (codes qx [M, K], scales dx [M, K/32]) and packed
+    weights, App. B.3 split into the integer GEMM term and the row-sum correction.
+
+    For 32-activation block b of weight group g = b // (group/32):
+      I[m, n, b] = sum_{j in b} qx[m, j] u[n, j]   (integer GEMM term)
+      R[m, b]    = sum_{j in b} qx[m, j]           (row-sum of the activations)
+      y[m, n]    = sum_b d[m, b] s[n, g] (I - o[n, g] R)    symmetric (o = 2^(q-1)) or zero point
+      y[m, n]    = sum_b d[m, b] (s[n, g] I + m[n, g] R)    fp16-minimum layout
+    The integers are exact, every block term is exact in binary64 (11-bit scales times
+    integers below 2^21) and the block sum is evaluated in binary64.
+    """
+    Q = np.asarray(qx, dtype=np.int64).reshape(-1, K)
+    M = Q.shape[0]
+    nb = K // Q8_BLOCK
+    per = group // Q8_BLOCK                                          # 32-blocks per weight group
+    u = unpack(codes, K, q).astype(np.int64)
+    if u.shape[0] != N:
+        raise ValueError("codes do not have N rows")
+    Qb = Q.reshape(M, nb, Q8_BLOCK)
+    I = np.einsum("mbj,nbj->mnb", Qb, u.reshape(N, nb, Q8_BLOCK))    # int64, exact
+    R = Qb.sum(axis=-1)                                              # [M, nb]
+    d = f16_bits_to_f64(dx).reshape(M, nb)
+    s = np.repeat(f16_bits_to_f64(scales).reshape(N, K // group), per, axis=1)   # [N, nb]
+    if mins is not None:
+        m = np.repeat(f16_bits_to_f64(mins).reshape(N, K // group), per, axis=1)
+        term = s[None] * I + m[None] * R[:, None, :]
+    else:
+        o = (np.full((N, nb), 1 << (q - 1), np.int64) if zp is None
+             else np.repeat(np.asarray(zp, np.int64).reshape(N, K // group), per, axis=1))
+        term = s[None] * (I - o[None] * R[:, None, :]).astype(np.float64)
+    return (d[:, None, :] * term).sum(axis=-1)

@@ -644,3 +644,104 @@ def test_diagnostics_tally_counts_groups():
                 n = int(((np.sign(d.margin) == sm) & (np.sign(d.gain) == sg)).sum())
                 assert d.tally[sm + 1, sg + 1] == n
         assert d.tally[1, 1] >= 4     # all-zero groups: no clipping either way
+
+
+# ---------------------------------------------------------------------------
+# Q8_0 activations and the integer-dot matmul (App. C, App. B.3).
+# ---------------------------------------------------------------------------
+
+def fl(r: Fr, p: int, emin: int) -> Fr:
+    """Round a rational to the binary format with p significant bits and minimum
+    normal exponent emin (gradual underflow), half to even; no overflow handling."""
+    if r == 0:
+        return Fr(0)
+    a = abs(r)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if a < Fr(2) ** e:
+        e -= 1
+    if a >= Fr(2) ** (e + 1):
+        e += 1
+    ulp = Fr(2) ** (max(e, emin) - p + 1)
+    v = rne(a / ulp) * ulp
+    return v if r > 0 else -v
+
+
+def f16_bits_of(r: Fr) -> int:
+    """binary16 bits of a value that is already representable (through Python's struct)."""
+    return struct.unpack("<H", struct.pack("<e", float(r)))[0]
+
+
+def test_q8_worked_example(golden_dir):
+    gold = json.load(open(os.path.join(golden_dir, "q8_worked_example.json")))
+    x = np.array([gold["x"]], np.float32)
+    assert np.array_equal(widen_bf16(synth.to_bf16_bits(x)), x)       # bf16 values
+    a = O.quantize_act_q8(x)
+    assert a.q.tolist() == [gold["q"]]
+    assert a.d.tolist() == [gold["d_f16_bits"]]
+
+
+def test_q8_activations_match_exact_rationals():
+    """Every code and scale against exact rational arithmetic: d = fl32(amax/127),
+    t = fl32(x/d), q = clip(rne(t)), stored binary16(d)."""
+    rng = np.random.default_rng(77)
+    x = rng.standard_t(3, size=(6, 256)) * 0.3
+    x[rng.random(x.shape) < 0.02] *= 40
+    x[0, :32] = np.arange(32) - 16.0                     # quotients near halves
+    x[1, 32:64] = 0.0                                    # zero block
+    x[2, 64:96] *= 1e-38                                 # tiny: subnormal d, binary16 scale 0
+    x = widen_bf16(synth.to_bf16_bits(x.astype(np.float32)))
+    a = O.quantize_act_q8(x)
+    for m in range(x.shape[0]):
+        for b in range(x.shape[1] // 32):
+            blk = [Fr(float(v)) for v in x[m, 32 * b:32 * b + 32]]
+            amax = max(abs(v) for v in blk)
+            d = fl(amax / 127, 24, -126)
+            assert a.d[m, b] == (f16_bits_of(fl(d, 11, -14)) if amax else 0)
+            for j, v in enumerate(blk):
+                want = 0 if amax == 0 else max(-127, min(127, rne(fl(v / d, 24, -126))))
+                assert a.q[m, 32 * b + j] == want, (m, b, j)
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("mode", [SIGNED, ASYM, ASYM_MIN])
+def test_matmul_q8_matches_exact_rationals(q, mode):
+    """y = sum_k (d q_x)[m, k] * W_hat[n, k] with every product and sum exact, against
+    the oracle's integer split (App. B.3) evaluated in binary64."""
+    rng = np.random.default_rng(100 * q + mode)
+    M, N, K, group = 2, 5, 128, 64
+    w = f32_groups(N, K, seed=q + 7 * mode)
+    r = O.quantize(w, group, q, mode)
+    x = widen_bf16(synth.to_bf16_bits((rng.standard_normal((M, K)) * 0.5).astype(np.float32)))
+    a = O.quantize_act_q8(x)
+    y = O.matmul_q8(a.q, a.d, r.codes, r.scales, r.zp, N, K, group, q, mins=r.mins)
+    u = O.unpack(r.codes, K, q)
+    s = [[Fr(float(v)) for v in row] for row in O.f16_bits_to_f64(r.scales)]
+    mins = O.f16_bits_to_f64(r.mins) if mode == ASYM_MIN else None
+    for m in range(M):
+        dx = [Fr(float(v)) for v in O.f16_bits_to_f64(a.d[m])]
+        for n in range(N):
+            exact = Fr(0)
+            for k in range(K):
+                g = k // group
+                if mode == ASYM_MIN:
+                    wk = s[n][g] * int(u[n, k]) + Fr(float(mins[n, g]))
+                else:
+                    o = int(r.zp[n, g]) if mode == ASYM else 1 << (q - 1)
+                    wk = s[n][g] * (int(u[n, k]) - o)
+                exact += dx[k // 32] * int(a.q[m, k]) * wk
+            assert abs(Fr(float(y[m, n])) - exact) <= abs(exact) * Fr(1, 2**50) + Fr(1, 2**80)
+
+
+def test_matmul_q8_equals_matmul_on_dequantized_activations():
+    """The integer split and the weight-only matmul of the dequantized activations
+    (d q exact in binary64) are the same sum."""
+    rng = np.random.default_rng(5)
+    w = bf16_groups(40, 512, seed=6)
+    x = widen_bf16(synth.to_bf16_bits((rng.standard_t(4, size=(3, 512)) * 0.2).astype(np.float32)))
+    a = O.quantize_act_q8(x)
+    xh = (a.q.reshape(3, 16, 32) * O.f16_bits_to_f64(a.d)[..., None]).reshape(3, 512)
+    for mode in (SIGNED, UNSIGNED, ASYM, ASYM_MIN):
+        r = O.quantize(w, 32, 4, mode)
+        y = O.matmul_q8(a.q, a.d, r.codes, r.scales, r.zp, 40, 512, 32, 4, mins=r.mins)
+        ref = O.matmul(xh, r.codes, r.scales, r.zp, 40, 512, 32, 4, mins=r.mins)
+        assert np.allclose(y, ref, rtol=1e-12, atol=1e-15)
