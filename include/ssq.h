@@ -239,6 +239,48 @@ int ssq_sign_diagnostics(const uint16_t* W, int64_t rows, int64_t cols, int grou
 int ssq_sign_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
                              int16_t* margin, float* gain, uint64_t* tally);
 
+/*
+ * ssq_quantize_act_q8 -- dynamic Q8_0 activation quantization (Sec. 5.2, App. C):
+ * per token and block of 32 activations the narrow-range symmetric grid
+ * {-127, ..., 127}, d = amax / 127 (binary32), q = clip(rne(x / d), -127, 127)
+ * computed from that d (Eq. (1) with z = 0), stored scale binary16(d); an all-zero
+ * block stores d = +0 and codes 0.
+ *
+ *   x      device, bf16 bits [M, K] row-major, read only (16-byte aligned)
+ *   M, K   tokens and activations per token; K a multiple of 32
+ *   q      device, int8 [M, K], written (16-byte aligned)
+ *   d      device, binary16 bits [M, K/32], written (2-byte aligned)
+ *   stream HIP stream the kernel is enqueued on (0 = null stream)
+ * Returns SSQ_OK or a negative ssq_status.
+ */
+int ssq_quantize_act_q8(const uint16_t* x, int64_t M, int64_t K, int8_t* q, uint16_t* d,
+                        hipStream_t stream);
+
+/*
+ * ssq_matmul_q8 -- y[M, N] = X W^T with Q8_0 activations and packed weights, by
+ * App. B.3's split into the integer GEMM term and the row-sum correction: for each
+ * block b of 32 activations inside weight group g,
+ *   I = sum_{j in b} qx[m, j] u[n, j],  R = sum_{j in b} qx[m, j]     (exact integers)
+ *   y[m, n] += d[m, b] s[n, g] (I - o[n, g] R)
+ * with o = 2^(q-1) (zp == NULL: the symmetric formats) or the zero point zp[n, g].
+ * Integer 4-way byte dot products; fp32 accumulation; y rounded to bf16 once.
+ * A decode kernel: each token streams the weights once (M = 1 is the target).
+ *
+ *   qx, dx codes and scales from ssq_quantize_act_q8 ([M, K] int8, 16-byte aligned;
+ *          [M, K/32] binary16, 2-byte aligned)
+ *   codes, scales, zp, N, K, group, q, y   as ssq_matmul
+ * Returns SSQ_OK or a negative ssq_status.
+ */
+int ssq_matmul_q8(const int8_t* qx, const uint16_t* dx, int64_t M, const uint8_t* codes,
+                  const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K, int group, int q,
+                  uint16_t* y, hipStream_t stream);
+
+/* ssq_matmul_q8 for the binary16-minimum layout: y[m, n] += d[m, b] (s[n, g] I +
+ * mins[n, g] R); mins as ssq_matmul_min (required when M, N > 0). */
+int ssq_matmul_q8_min(const int8_t* qx, const uint16_t* dx, int64_t M, const uint8_t* codes,
+                      const uint16_t* scales, const uint16_t* mins, int64_t N, int64_t K, int group,
+                      int q, uint16_t* y, hipStream_t stream);
+
 /* Static description of a status code; never NULL. */
 const char* ssq_strerror(int status);
 

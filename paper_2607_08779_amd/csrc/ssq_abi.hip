@@ -78,6 +78,22 @@ int dispatch_bf16(const uint16_t* x, int64_t M, const uint8_t* codes, const uint
                                          workspace_bytes, stream));
 }
 
+int check_act_q8(const void* x, int64_t M, int64_t K, const void* q, const uint16_t* d) {
+  if (M < 0 || K < 0 || M > kMaxDim || K > kMaxDim || K % 32 != 0 || M * K > kMaxElems) return SSQ_EINVAL;
+  if (M == 0 || K == 0) return SSQ_OK;
+  if (x == nullptr || q == nullptr || d == nullptr) return SSQ_EINVAL;
+  if (!aligned(x, 16) || !aligned(q, 16) || !aligned(d, 2)) return SSQ_EALIGN;
+  return SSQ_OK;
+}
+
+int check_matmul_q8(const int8_t* qx, const uint16_t* dx, int64_t M, const uint8_t* codes,
+                    const uint16_t* scales, int64_t N, int64_t K, int group, int q, const uint16_t* y) {
+  const int st = check_matmul(qx, M, codes, scales, N, K, group, q, y);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  if (dx == nullptr) return SSQ_EINVAL;
+  return aligned(dx, 2) ? SSQ_OK : SSQ_EALIGN;
+}
+
 // Shared checks of the binary16-minimum entry points: a minimum per group, 2-byte aligned.
 int check_mins(const uint16_t* mins, bool needed) {
   if (!needed) return SSQ_OK;
@@ -193,6 +209,30 @@ int ssq_sign_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int gro
   const int st = check_diagnostics(W, rows, cols, group, q, margin, gain, tally);
   if (st != SSQ_OK || ((rows == 0 || cols == 0) && tally == nullptr)) return st;
   return status_of(ssq::launch_diagnostics_f32(W, rows, cols, group, q, margin, gain, tally));
+}
+
+int ssq_quantize_act_q8(const uint16_t* x, int64_t M, int64_t K, int8_t* q, uint16_t* d,
+                        hipStream_t stream) {
+  const int st = check_act_q8(x, M, K, q, d);
+  if (st != SSQ_OK || M == 0 || K == 0) return st;
+  return status_of(ssq::launch_quantize_act_q8(x, M, K, q, d, stream));
+}
+
+int ssq_matmul_q8(const int8_t* qx, const uint16_t* dx, int64_t M, const uint8_t* codes,
+                  const uint16_t* scales, const uint8_t* zp, int64_t N, int64_t K, int group, int q,
+                  uint16_t* y, hipStream_t stream) {
+  const int st = check_matmul_q8(qx, dx, M, codes, scales, N, K, group, q, y);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  return status_of(ssq::launch_matmul_q8(qx, dx, M, codes, scales, zero_points(zp), N, K, group, q, y, stream));
+}
+
+int ssq_matmul_q8_min(const int8_t* qx, const uint16_t* dx, int64_t M, const uint8_t* codes,
+                      const uint16_t* scales, const uint16_t* mins, int64_t N, int64_t K, int group, int q,
+                      uint16_t* y, hipStream_t stream) {
+  int st = check_matmul_q8(qx, dx, M, codes, scales, N, K, group, q, y);
+  if (st == SSQ_OK) st = check_mins(mins, M > 0 && N > 0);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  return status_of(ssq::launch_matmul_q8(qx, dx, M, codes, scales, minimums(mins), N, K, group, q, y, stream));
 }
 
 const char* ssq_strerror(int status) {

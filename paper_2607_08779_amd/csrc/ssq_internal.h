@@ -216,4 +216,11 @@ hipError_t launch_diagnostics_bf16(const uint16_t* W, int64_t rows, int64_t cols
 hipError_t launch_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
                                   int16_t* margin, float* gain, uint64_t* tally);
 
+// Q8_0 activations and the integer-dot matmul (q8.hip).
+hipError_t launch_quantize_act_q8(const uint16_t* x, int64_t M, int64_t K, int8_t* q, uint16_t* d,
+                                  hipStream_t stream);
+hipError_t launch_matmul_q8(const int8_t* qx, const uint16_t* dx, int64_t M, const uint8_t* codes,
+                            const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K, int group, int q,
+                            uint16_t* y, hipStream_t stream);
+
 }  // namespace ssq

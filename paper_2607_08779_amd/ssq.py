@@ -49,6 +49,10 @@ for _name in ("ssq_matmul_min", "ssq_matmul_min_f32", "ssq_matmul_min_ws"):
     _EXPORTS[_name] = (ctypes.c_int, list(_EXPORTS[_name.replace("_min", "")][1]))
 _EXPORTS["ssq_sign_diagnostics"] = _Q_MIN
 _EXPORTS["ssq_sign_diagnostics_f32"] = _Q_MIN
+_EXPORTS["ssq_quantize_act_q8"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p])
+_EXPORTS["ssq_matmul_q8"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p] + _EXPORTS["ssq_matmul"][1][1:])
+_EXPORTS["ssq_matmul_q8_min"] = _EXPORTS["ssq_matmul_q8"]
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -214,3 +218,38 @@ def ssq_sign_diagnostics(W: torch.Tensor, group: int, q: int, tally: bool = True
     st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(margin), _ptr(gain), _ptr(t))
     _check(fn, st)
     return margin, gain, (t.view(3, 3) if t is not None else None)
+
+
+def ssq_quantize_act_q8(x: torch.Tensor, out=None):
+    """Dynamic Q8_0 quantization of bf16 activations x [M, K] (App. C) on the current
+    stream: returns (codes int8 [M, K], scales int16 [M, K/32] holding binary16 bits).
+    ``out`` = (codes, scales) reuses buffers."""
+    if x.dim() != 2 or not x.is_contiguous() or x.dtype != torch.bfloat16:
+        raise ValueError("x must be a contiguous bfloat16 [M, K] tensor")
+    M, K = x.shape
+    if out is None:
+        qx = torch.empty((M, K), dtype=torch.int8, device=x.device)
+        dx = torch.empty((M, K // 32), dtype=torch.int16, device=x.device)
+    else:
+        qx, dx = out
+    _check("ssq_quantize_act_q8", lib().ssq_quantize_act_q8(_ptr(x), M, K, _ptr(qx), _ptr(dx), _stream(x.device)))
+    return qx, dx
+
+
+def ssq_matmul_q8(qx: torch.Tensor, dx: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
+                  zp: Optional[torch.Tensor], N: int, K: int, group: int, q: int,
+                  out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """y [M, N] bf16 from Q8_0 activations (``ssq_quantize_act_q8``) and packed weights
+    by integer dot products (App. B.3), on the current stream.  ``zp``: None
+    (symmetric), uint8 zero points, or int16 binary16 minimums (``ssq_matmul_q8_min``)."""
+    if qx.dim() != 2 or not qx.is_contiguous() or qx.dtype != torch.int8 or qx.shape[1] != K:
+        raise ValueError("qx must be a contiguous int8 [M, K] tensor")
+    if zp is not None and zp.dtype not in (torch.uint8, torch.int16):
+        raise TypeError("zp must be uint8 zero points or int16 binary16 minimums")
+    fn = "ssq_matmul_q8_min" if zp is not None and zp.dtype == torch.int16 else "ssq_matmul_q8"
+    M = qx.shape[0]
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=qx.device) if out is None else out
+    st = getattr(lib(), fn)(_ptr(qx), _ptr(dx), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
+                            _ptr(y), _stream(qx.device))
+    _check(fn, st)
+    return y

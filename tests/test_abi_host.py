@@ -25,7 +25,9 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_matmul_min",
                                     "ssq_matmul_min_f32", "ssq_matmul_min_ws",
-                                    "ssq_matmul_workspace_size", "ssq_matmul_ws", "ssq_quantize",
+                                    "ssq_matmul_q8", "ssq_matmul_q8_min",
+                                    "ssq_matmul_workspace_size", "ssq_matmul_ws",
+                                    "ssq_quantize", "ssq_quantize_act_q8",
                                     "ssq_quantize_f32", "ssq_quantize_min", "ssq_quantize_min_f32",
                                     "ssq_sign_diagnostics", "ssq_sign_diagnostics_f32",
                                     "ssq_strerror"]
@@ -190,3 +192,37 @@ def test_binding_refuses_host_tensors():
         ssq.ssq_quantize(W, 32, 4, ssq.SIGNED_SYM)
     with pytest.raises(ValueError, match="GPU tensors"):
         ssq.ssq_sign_diagnostics(W, 32, 4)
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(K=48), EINVAL), (dict(M=-1), EINVAL), (dict(x=None), EINVAL), (dict(q=None), EINVAL),
+    (dict(d=None), EINVAL), (dict(x=P2), EALIGN), (dict(q=P2), EALIGN),
+    (dict(d=ctypes.c_void_p((1 << 20) + 1)), EALIGN),
+])
+def test_quantize_act_q8_rejects_invalid_arguments(args, status):
+    a = dict(x=P16, M=2, K=64, q=P16, d=P16)
+    a.update(args)
+    assert ssq.lib().ssq_quantize_act_q8(a["x"], a["M"], a["K"], a["q"], a["d"], None) == status
+
+
+def test_quantize_act_q8_empty_is_a_no_op():
+    assert ssq.lib().ssq_quantize_act_q8(None, 0, 64, None, None, None) == 0
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(q=5), EINVAL), (dict(group=16), EINVAL), (dict(K=48), EINVAL), (dict(K=1 << 23), EINVAL),
+    (dict(qx=None), EINVAL), (dict(dx=None), EINVAL), (dict(codes=None), EINVAL), (dict(y=None), EINVAL),
+    (dict(qx=P2), EALIGN), (dict(codes=P2), EALIGN), (dict(dx=ctypes.c_void_p((1 << 20) + 1)), EALIGN),
+])
+def test_matmul_q8_rejects_invalid_arguments(args, status):
+    a = dict(qx=P16, dx=P16, M=1, codes=P16, scales=P16, zp=None, N=4, K=64, group=32, q=4, y=P16)
+    a.update(args)
+    lib = ssq.lib()
+    assert lib.ssq_matmul_q8(a["qx"], a["dx"], a["M"], a["codes"], a["scales"], a["zp"], a["N"], a["K"],
+                             a["group"], a["q"], a["y"], None) == status
+    assert lib.ssq_matmul_q8_min(a["qx"], a["dx"], a["M"], a["codes"], a["scales"], P16, a["N"], a["K"],
+                                 a["group"], a["q"], a["y"], None) == status
+
+
+def test_matmul_q8_min_requires_minimums():
+    assert ssq.lib().ssq_matmul_q8_min(P16, P16, 1, P16, P16, None, 4, 64, 32, 4, P16, None) == EINVAL

@@ -1,0 +1,128 @@
+"""GPU parity: Q8_0 activation quantization (bit-exact codes and scales) and the
+integer-dot matmul (App. B.3) against the CPU oracle (App. C readings)."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import ssq_oracle as O
+from paper_2607_08779_amd import ssq, synth
+from tests.parity_common import log_metric, rel_l2, sample_rows, to_device, y_to_f64
+
+pytestmark = pytest.mark.gpu
+
+MODES = [O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM, O.ASYM_MIN]
+
+
+def bf16_bits(a):
+    return synth.to_bf16_bits(np.asarray(a, np.float32))
+
+
+def act_bits(M, K, seed, scale=1.0):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_t(4, size=(M, K)) * scale
+    x[rng.random(x.shape) < 0.01] *= 30
+    return bf16_bits(x)
+
+
+def check_act(xb, tag=""):
+    qx, dx = ssq.ssq_quantize_act_q8(to_device(xb, True))
+    torch.cuda.synchronize()
+    with np.errstate(over="ignore"):
+        ref = O.quantize_act_q8(O.bf16_bits_to_f32(xb))
+    q, d = qx.cpu().numpy(), dx.cpu().numpy().view(np.uint16)
+    if not np.array_equal(q, ref.q):
+        m, k = np.argwhere(q != ref.q)[0]
+        raise AssertionError(f"{tag}: code ({m}, {k}) gpu {q[m, k]} oracle {ref.q[m, k]}")
+    if not np.array_equal(d, ref.d):
+        m, b = np.argwhere(d != ref.d)[0]
+        raise AssertionError(f"{tag}: scale ({m}, {b}) gpu {d[m, b]:#06x} oracle {ref.d[m, b]:#06x}")
+    return qx, dx, ref
+
+
+@pytest.mark.parametrize("M,K", [(1, 32), (1, 4096), (3, 14336), (64, 1024)])
+def test_quantize_act_q8_matches_oracle(M, K):
+    check_act(act_bits(M, K, seed=M * 7 + K), tag=f"M={M} K={K}")
+
+
+def test_quantize_act_q8_worked_example_and_edges():
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "q8_worked_example.json")))
+    _, _, ref = check_act(bf16_bits([gold["x"]]), tag="worked example")
+    assert ref.q.tolist() == [gold["q"]]
+    rng = np.random.default_rng(4)
+    rows = [np.zeros(64), -np.zeros(64), rng.standard_normal(64) * 1e-38,   # subnormal d, binary16 0
+            rng.standard_normal(64) * 3e7,                                  # binary16 scale overflows
+            np.arange(64) - 31.5, np.full(64, -2.75)]
+    check_act(bf16_bits(np.stack(rows)), tag="edges")
+
+
+def check_q8_matmul(w, x_bits, group, q, mode, rows_idx=None, tag=""):
+    """Oracle-quantized weights and activations on the GPU through ssq_matmul_q8."""
+    N, K = w.shape
+    r = O.quantize(w, group, q, mode)
+    a = O.quantize_act_q8(O.bf16_bits_to_f32(x_bits))
+    meta = r.mins if mode == O.ASYM_MIN else r.zp
+    dev_meta = None if meta is None else torch.from_numpy(
+        meta.view(np.int16) if mode == O.ASYM_MIN else meta).cuda()
+    y = ssq.ssq_matmul_q8(torch.from_numpy(a.q).cuda(), torch.from_numpy(a.d.view(np.int16)).cuda(),
+                          torch.from_numpy(r.codes).cuda(), torch.from_numpy(r.scales.view(np.int16)).cuda(),
+                          dev_meta, N, K, group, q)
+    torch.cuda.synchronize()
+    sel = slice(None) if rows_idx is None else rows_idx
+    ref = O.matmul_q8(a.q, a.d, r.codes[sel], r.scales[sel], None if r.zp is None else r.zp[sel],
+                      r.codes[sel].shape[0], K, group, q, mins=None if r.mins is None else r.mins[sel])
+    got = y_to_f64(y)[:, sel]
+    # bf16 output rounding (2^-9 relative) plus fp32 accumulation over K/32 block terms
+    tol = 2.0 ** -8 * np.abs(ref) + 1e-5 * np.abs(ref).max(axis=1, keepdims=True) + 1e-30
+    bad = np.abs(got - ref) > tol
+    err = rel_l2(got, ref)
+    log_metric(test="q8_matmul", tag=tag, rel_l2=err)
+    assert not bad.any(), f"{tag}: {bad.sum()} outputs off, first {np.argwhere(bad)[0]}, rel L2 {err:.2e}"
+    assert err <= 5e-3, f"{tag}: rel L2 {err:.2e}"
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("mode", MODES)
+def test_matmul_q8_all_formats(q, group, mode):
+    rng = np.random.default_rng(q * 31 + group + mode)
+    w = O.bf16_bits_to_f32(bf16_bits(rng.standard_t(5, size=(37, 1024)) * 0.02))
+    check_q8_matmul(w, act_bits(2, 1024, seed=q + group), group, q, mode, tag=f"q={q} g={group} m={mode}")
+
+
+@pytest.mark.parametrize("K", [32, 96, 19200])
+def test_matmul_q8_reduction_lengths(K):
+    """One block, an odd block count, and 600 blocks (two passes, the second ragged)."""
+    rng = np.random.default_rng(K)
+    w = O.bf16_bits_to_f32(bf16_bits(rng.standard_t(5, size=(9, K)) * 0.02))
+    for q in (2, 3, 4):
+        check_q8_matmul(w, act_bits(1, K, seed=K + q), 32, q, O.SIGNED_SYM, tag=f"K={K} q={q}")
+
+
+@pytest.mark.parametrize("M", [1, 2, 5])
+def test_matmul_q8_token_counts(M):
+    rng = np.random.default_rng(M)
+    w = O.bf16_bits_to_f32(bf16_bits(rng.standard_t(5, size=(70, 2048)) * 0.02))
+    check_q8_matmul(w, act_bits(M, 2048, seed=M), 32, 4, O.ASYM, tag=f"M={M}")
+
+
+def test_q8_pipeline_llama3_8b_down_proj_full_size():
+    """4096x14336 at W4 g32, signed: GPU weight quantization, GPU activation
+    quantization and the integer matmul against the oracle on sampled rows."""
+    spec = synth.llama3_8b_decode().layers["down_proj"]
+    wb = synth.weights(spec)
+    x = act_bits(1, spec.cols, seed=21, scale=0.5)
+    W = to_device(wb, True)
+    codes, scales, zp = ssq.ssq_quantize(W, 32, 4, O.SIGNED_SYM)
+    qx, dx, a = check_act(x, tag="down_proj activations")
+    y = ssq.ssq_matmul_q8(qx, dx, codes, scales, zp, spec.rows, spec.cols, 32, 4)
+    torch.cuda.synchronize()
+    rows = sample_rows(spec.rows, 64, seed=5)
+    r = O.quantize(O.bf16_bits_to_f32(wb[rows]), 32, 4, O.SIGNED_SYM)
+    assert np.array_equal(codes.cpu().numpy()[rows], r.codes)
+    ref = O.matmul_q8(a.q, a.d, r.codes, r.scales, None, len(rows), spec.cols, 32, 4)
+    err = rel_l2(y_to_f64(y)[:, rows], ref)
+    log_metric(test="q8_pipeline_full", rel_l2=err)
+    assert err <= 5e-3, err
