@@ -182,6 +182,7 @@ constexpr int kSplitWaves = 8;                 // 16 weight rows each
 constexpr int kSplitRows = 16 * kSplitWaves;
 constexpr int kChunk = 8;                      // super-blocks whose loads are in flight at once
 constexpr int kSplitTargetWorkgroups = 512;    // two per CU
+static_assert(kChunk == kSplitWaves, "wavefront w stages super-block w of a chunk");
 constexpr int kSplitMaxSplits = 64;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
