@@ -240,6 +240,24 @@ int ssq_sign_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int gro
                              int16_t* margin, float* gain, uint64_t* tally);
 
 /*
+ * ssq_quantize_diag -- ssq_quantize with mode SSQ_SIGNED_SYM fused with the
+ * sign-rule margin and gain of ssq_sign_diagnostics (Sec. 4 Remark 1): one pass over
+ * W writes the same codes and scales as ssq_quantize and the same margin and gain as
+ * ssq_sign_diagnostics (no tally: count the outputs, or call ssq_sign_diagnostics).
+ *
+ *   W, rows, cols, group, q, codes, scales   as ssq_quantize (signed symmetric)
+ *   margin device, int16 [rows, cols/group], written (2-byte aligned)
+ *   gain   device, float [rows, cols/group], written (4-byte aligned)
+ * Enqueued on the null stream.  Returns SSQ_OK or a negative ssq_status.
+ */
+int ssq_quantize_diag(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                      uint8_t* codes, uint16_t* scales, int16_t* margin, float* gain);
+
+/* ssq_quantize_diag for binary32 weights W[rows, cols]; otherwise identical. */
+int ssq_quantize_diag_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                          uint8_t* codes, uint16_t* scales, int16_t* margin, float* gain);
+
+/*
  * ssq_quantize_act_q8 -- dynamic Q8_0 activation quantization (Sec. 5.2, App. C):
  * per token and block of 32 activations the narrow-range symmetric grid
  * {-127, ..., 127}, d = amax / 127 (binary32), q = clip(rne(x / d), -127, 127)

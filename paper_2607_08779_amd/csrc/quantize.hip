@@ -11,6 +11,10 @@
 // weights is G/8 consecutive lanes of one wavefront, which reduce max/min with
 // butterfly shuffles.  Each lane quantizes its 8 weights and packs them into
 // 8q bits; neighbouring lanes merge those bits so every store is a dword.
+//
+// DIAG (signed grid only) also stores each group's sign-rule margin and gain (Sec. 4
+// Remark 1, sign_stats.h) from the same registers: one pass over the weights.
+#include "sign_stats.h"
 #include "ssq_internal.h"
 
 namespace ssq {
@@ -64,12 +68,15 @@ __device__ __forceinline__ void store_codes(uint8_t* codes, int64_t chunk, uint3
   }
 }
 
-template <typename In, int Q, int G, int MODE>
+template <typename In, int Q, int G, int MODE, bool DIAG = false>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict__ W,
                                                             int64_t total_chunks,
                                                             uint8_t* __restrict__ codes,
                                                             uint16_t* __restrict__ scales,
-                                                            void* __restrict__ meta) {
+                                                            void* __restrict__ meta,
+                                                            int16_t* __restrict__ margin = nullptr,
+                                                            float* __restrict__ gain = nullptr) {
+  static_assert(!DIAG || MODE == 0, "the diagnostics describe the signed grid");
   constexpr int kLanesPerGroup = G / 8;
   constexpr float kLo = -(float)(1 << (Q - 1));          // min A_q (signed alphabet)
   constexpr float kHi = (float)((1 << (Q - 1)) - 1);     // max A_q
@@ -98,6 +105,9 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
     for (int i = 1; i < 8; ++i) { mx = fmaxf(mx, w[u][i]); mn = fminf(mn, w[u][i]); }
     mx = group_max<kLanesPerGroup>(mx);            // max_j w_j over the group
     const float nmn = group_max<kLanesPerGroup>(-mn);  // -min_j w_j
+    int diag_m = 0;
+    double diag_g = 0.0;
+    if constexpr (DIAG) sign_stats<Q, G>(w[u], mx, nmn, diag_m, diag_g);
 
     uint32_t packed = 0;
     uint16_t scale_bits = 0;
@@ -197,6 +207,10 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
       scales[chunk / kLanesPerGroup] = scale_bits;
       if constexpr (MODE == 2) static_cast<uint8_t*>(meta)[chunk / kLanesPerGroup] = zero_point;
       if constexpr (MODE == 3) static_cast<uint16_t*>(meta)[chunk / kLanesPerGroup] = min_bits;
+      if constexpr (DIAG) {
+        margin[chunk / kLanesPerGroup] = (int16_t)diag_m;
+        gain[chunk / kLanesPerGroup] = (float)diag_g;
+      }
     }
   }
 }
@@ -225,6 +239,35 @@ hipError_t launch_group(const In* W, int64_t total_chunks, int group, int mode, 
   }
 }
 
+template <typename In, int Q, int G>
+hipError_t launch_diag(const In* W, int64_t total_chunks, uint8_t* codes, uint16_t* scales, int16_t* margin,
+                       float* gain, hipStream_t stream) {
+  const int64_t per_block = (int64_t)kThreads * kUnroll;
+  const dim3 grid((unsigned)((total_chunks + per_block - 1) / per_block));
+  quantize_kernel<In, Q, G, 0, true><<<grid, kThreads, 0, stream>>>(W, total_chunks, codes, scales, nullptr,
+                                                                   margin, gain);
+  return hipGetLastError();
+}
+
+template <typename In>
+hipError_t launch_diag_any(const In* W, int64_t rows, int64_t cols, int group, int q, uint8_t* codes,
+                           uint16_t* scales, int16_t* margin, float* gain, hipStream_t stream) {
+  const int64_t total_chunks = rows * cols / 8;
+  if (total_chunks == 0) return hipSuccess;
+  switch (q * 1000 + group) {
+    case 2032: return launch_diag<In, 2, 32>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 2064: return launch_diag<In, 2, 64>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 2128: return launch_diag<In, 2, 128>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 3032: return launch_diag<In, 3, 32>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 3064: return launch_diag<In, 3, 64>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 3128: return launch_diag<In, 3, 128>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 4032: return launch_diag<In, 4, 32>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 4064: return launch_diag<In, 4, 64>(W, total_chunks, codes, scales, margin, gain, stream);
+    case 4128: return launch_diag<In, 4, 128>(W, total_chunks, codes, scales, margin, gain, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <typename In>
 hipError_t launch_any(const In* W, int64_t rows, int64_t cols, int group, int q, int mode,
                       uint8_t* codes, uint16_t* scales, void* zp, hipStream_t stream) {
@@ -249,6 +292,18 @@ hipError_t launch_quantize_f32(const float* W, int64_t rows, int64_t cols, int g
                                int mode, uint8_t* codes, uint16_t* scales, void* zp,
                                hipStream_t stream) {
   return launch_any<float>(W, rows, cols, group, q, mode, codes, scales, zp, stream);
+}
+
+hipError_t launch_quantize_diag_bf16(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                                     uint8_t* codes, uint16_t* scales, int16_t* margin, float* gain,
+                                     hipStream_t stream) {
+  return launch_diag_any<uint16_t>(W, rows, cols, group, q, codes, scales, margin, gain, stream);
+}
+
+hipError_t launch_quantize_diag_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                                    uint8_t* codes, uint16_t* scales, int16_t* margin, float* gain,
+                                    hipStream_t stream) {
+  return launch_diag_any<float>(W, rows, cols, group, q, codes, scales, margin, gain, stream);
 }
 
 }  // namespace ssq

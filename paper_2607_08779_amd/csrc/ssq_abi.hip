@@ -211,6 +211,24 @@ int ssq_sign_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int gro
   return status_of(ssq::launch_diagnostics_f32(W, rows, cols, group, q, margin, gain, tally));
 }
 
+int ssq_quantize_diag(const uint16_t* W, int64_t rows, int64_t cols, int group, int q, uint8_t* codes,
+                      uint16_t* scales, int16_t* margin, float* gain) {
+  int st = check_quantize(W, rows, cols, group, q, SSQ_SIGNED_SYM, codes, scales, nullptr);
+  if (st == SSQ_OK && rows > 0 && cols > 0)
+    st = margin == nullptr || gain == nullptr ? SSQ_EINVAL : !aligned(margin, 2) || !aligned(gain, 4) ? SSQ_EALIGN : SSQ_OK;
+  if (st != SSQ_OK || rows == 0 || cols == 0) return st;
+  return status_of(ssq::launch_quantize_diag_bf16(W, rows, cols, group, q, codes, scales, margin, gain, nullptr));
+}
+
+int ssq_quantize_diag_f32(const float* W, int64_t rows, int64_t cols, int group, int q, uint8_t* codes,
+                          uint16_t* scales, int16_t* margin, float* gain) {
+  int st = check_quantize(W, rows, cols, group, q, SSQ_SIGNED_SYM, codes, scales, nullptr);
+  if (st == SSQ_OK && rows > 0 && cols > 0)
+    st = margin == nullptr || gain == nullptr ? SSQ_EINVAL : !aligned(margin, 2) || !aligned(gain, 4) ? SSQ_EALIGN : SSQ_OK;
+  if (st != SSQ_OK || rows == 0 || cols == 0) return st;
+  return status_of(ssq::launch_quantize_diag_f32(W, rows, cols, group, q, codes, scales, margin, gain, nullptr));
+}
+
 int ssq_quantize_act_q8(const uint16_t* x, int64_t M, int64_t K, int8_t* q, uint16_t* d,
                         hipStream_t stream) {
   const int st = check_act_q8(x, M, K, q, d);

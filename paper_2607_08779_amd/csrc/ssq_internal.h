@@ -216,6 +216,14 @@ hipError_t launch_diagnostics_bf16(const uint16_t* W, int64_t rows, int64_t cols
 hipError_t launch_diagnostics_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
                                   int16_t* margin, float* gain, uint64_t* tally);
 
+// Signed quantization fused with the sign-rule margin and gain (quantize.hip).
+hipError_t launch_quantize_diag_bf16(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,
+                                     uint8_t* codes, uint16_t* scales, int16_t* margin, float* gain,
+                                     hipStream_t stream);
+hipError_t launch_quantize_diag_f32(const float* W, int64_t rows, int64_t cols, int group, int q,
+                                    uint8_t* codes, uint16_t* scales, int16_t* margin, float* gain,
+                                    hipStream_t stream);
+
 // Q8_0 activations and the integer-dot matmul (q8.hip).
 hipError_t launch_quantize_act_q8(const uint16_t* x, int64_t M, int64_t K, int8_t* q, uint16_t* d,
                                   hipStream_t stream);

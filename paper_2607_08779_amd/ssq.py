@@ -49,6 +49,9 @@ for _name in ("ssq_matmul_min", "ssq_matmul_min_f32", "ssq_matmul_min_ws"):
     _EXPORTS[_name] = (ctypes.c_int, list(_EXPORTS[_name.replace("_min", "")][1]))
 _EXPORTS["ssq_sign_diagnostics"] = _Q_MIN
 _EXPORTS["ssq_sign_diagnostics_f32"] = _Q_MIN
+_EXPORTS["ssq_quantize_diag"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                                                ctypes.c_int] + [ctypes.c_void_p] * 4)
+_EXPORTS["ssq_quantize_diag_f32"] = _EXPORTS["ssq_quantize_diag"]
 _EXPORTS["ssq_quantize_act_q8"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p])
 _EXPORTS["ssq_matmul_q8"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p] + _EXPORTS["ssq_matmul"][1][1:])
@@ -253,3 +256,25 @@ def ssq_matmul_q8(qx: torch.Tensor, dx: torch.Tensor, codes: torch.Tensor, scale
                             _ptr(y), _stream(qx.device))
     _check(fn, st)
     return y
+
+
+def ssq_quantize_diag(W: torch.Tensor, group: int, q: int):
+    """Signed-symmetric quantization fused with the sign-rule statistics (Sec. 4
+    Remark 1): returns (codes, scales, margin int16, gain float32) in one pass over W,
+    on the null stream."""
+    if W.dim() != 2 or not W.is_contiguous():
+        raise ValueError("W must be a contiguous 2-D tensor")
+    if W.dtype == torch.bfloat16:
+        fn = "ssq_quantize_diag"
+    elif W.dtype == torch.float32:
+        fn = "ssq_quantize_diag_f32"
+    else:
+        raise TypeError("W must be bfloat16 or float32")
+    rows, cols = W.shape
+    groups = cols // group if group else 0
+    codes = torch.empty((rows, cols * q // 8), dtype=torch.uint8, device=W.device)
+    scales = torch.empty((rows, groups), dtype=torch.int16, device=W.device)
+    margin = torch.empty((rows, groups), dtype=torch.int16, device=W.device)
+    gain = torch.empty((rows, groups), dtype=torch.float32, device=W.device)
+    _check(fn, getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(codes), _ptr(scales), _ptr(margin), _ptr(gain)))
+    return codes, scales, margin, gain

@@ -28,6 +28,7 @@ def test_header_declares_the_boundary():
                                     "ssq_matmul_q8", "ssq_matmul_q8_min",
                                     "ssq_matmul_workspace_size", "ssq_matmul_ws",
                                     "ssq_quantize", "ssq_quantize_act_q8",
+                                    "ssq_quantize_diag", "ssq_quantize_diag_f32",
                                     "ssq_quantize_f32", "ssq_quantize_min", "ssq_quantize_min_f32",
                                     "ssq_sign_diagnostics", "ssq_sign_diagnostics_f32",
                                     "ssq_strerror"]
@@ -226,3 +227,16 @@ def test_matmul_q8_rejects_invalid_arguments(args, status):
 
 def test_matmul_q8_min_requires_minimums():
     assert ssq.lib().ssq_matmul_q8_min(P16, P16, 1, P16, P16, None, 4, 64, 32, 4, P16, None) == EINVAL
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(q=5), EINVAL), (dict(group=16), EINVAL), (dict(cols=48), EINVAL), (dict(W=None), EINVAL),
+    (dict(codes=None), EINVAL), (dict(margin=None), EINVAL), (dict(gain=None), EINVAL),
+    (dict(W=P2), EALIGN), (dict(margin=ctypes.c_void_p((1 << 20) + 1)), EALIGN), (dict(gain=P2), EALIGN),
+])
+def test_quantize_diag_rejects_invalid_arguments(args, status):
+    a = dict(W=P16, rows=4, cols=64, group=32, q=4, codes=P16, scales=P16, margin=P16, gain=P16)
+    a.update(args)
+    for fn in (ssq.lib().ssq_quantize_diag, ssq.lib().ssq_quantize_diag_f32):
+        assert fn(a["W"], a["rows"], a["cols"], a["group"], a["q"], a["codes"], a["scales"], a["margin"],
+                  a["gain"]) == status

@@ -97,3 +97,36 @@ def test_diagnostics_empty():
     torch.cuda.synchronize()
     assert margin.shape == (0, 2) and gain.shape == (0, 2)
     assert tally.cpu().numpy().sum() == 0
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("bf16", [True, False])
+def test_quantize_diag_matches_both_oracles(q, group, bf16):
+    """The fused kernel: codes and scales of the signed grid and the sign-rule margin and
+    gain, each against its own oracle."""
+    rng = np.random.default_rng(q * 10 + group + bf16)
+    w = rng.standard_t(4, size=(23, 1024)) * 0.02
+    w[rng.random(w.shape) < 0.01] *= 20
+    w_host = synth.to_bf16_bits(w.astype(np.float32)) if bf16 else w.astype(np.float32)
+    codes, scales, margin, gain = ssq.ssq_quantize_diag(to_device(w_host, bf16), group, q)
+    torch.cuda.synchronize()
+    wf = widen(w_host, bf16)
+    r = O.quantize(wf, group, q, O.SIGNED_SYM)
+    d = O.sign_diagnostics(wf, group, q)
+    assert np.array_equal(codes.cpu().numpy(), r.codes)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint16), r.scales)
+    assert np.array_equal(margin.cpu().numpy(), d.margin)
+    assert np.array_equal(gain.cpu().numpy(), d.gain)
+
+
+def test_quantize_diag_full_size_sampled():
+    spec = synth.llama3_8b_decode().layers["down_proj"]
+    w = synth.weights(spec)
+    codes, scales, margin, gain = ssq.ssq_quantize_diag(to_device(w, True), 32, 4)
+    m2, g2, _ = ssq.ssq_sign_diagnostics(to_device(w, True), 32, 4, tally=False)
+    torch.cuda.synchronize()
+    assert torch.equal(margin, m2) and torch.equal(gain.view(torch.int32), g2.view(torch.int32))
+    rows = sample_rows(spec.rows, 32, seed=9)
+    r = O.quantize(widen(w[rows], True), 32, 4, O.SIGNED_SYM)
+    assert np.array_equal(codes.cpu().numpy()[rows], r.codes)
