@@ -209,6 +209,47 @@ def diagnostics_bytes(N, K, g):
     return 2 * N * K + 6 * N * K // g
 
 
+def stream_ceiling(torch, dev, nbytes: int, copies: int, reps: int):
+    """The practical HBM ceiling next to the GEMV: a plain streaming read (the
+    measurement-only ssq_bench_stream_read kernel) of `copies` distinct buffers of the
+    GEMV's byte count, replayed in a HIP graph like the GEMV phase.  None if the
+    measurement library is not built."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2607_08779_amd", "libssq_bench.so")
+    if not os.path.exists(path):
+        return None
+    lib = ctypes.CDLL(path)
+    lib.ssq_bench_stream_read.restype = ctypes.c_int
+    lib.ssq_bench_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    bufs = [torch.full((nbytes // 4,), i + 1, dtype=torch.int32, device=dev) for i in range(copies)]
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        def run():
+            for b in bufs:
+                st = lib.ssq_bench_stream_read(b.data_ptr(), nbytes, sink.data_ptr(), s.cuda_stream)
+                if st != 0:
+                    raise RuntimeError(f"ssq_bench_stream_read failed ({st})")
+        run()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            run()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        for _ in range(reps):
+            g.replay()
+        e1.record(s)
+        torch.cuda.synchronize()
+    avg = e0.elapsed_time(e1) / 1e3 / (reps * copies)
+    del bufs
+    return {"kernel": "stream_read_kernel (measurement only)", "bytes_per_launch": nbytes,
+            "avg_launch_us": round(avg * 1e6, 3), "gbs": round(nbytes / avg / 1e9, 2),
+            "frac": round(nbytes / avg / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def sweep(args) -> int:
     """Throughput of every format on the Llama3 shapes (event-timed; weights past the
     Infinity Cache for the decode passes).  One JSON line with a row per case."""
@@ -499,6 +540,14 @@ def main() -> int:
         if not torch.equal(y_eager.view(torch.int16), y1.view(torch.int16)):
             raise RuntimeError("graph replay of the GEMV differs from an eager launch")
 
+    def spread(i, per_step):
+        """Median per-launch time (us) and coefficient of variation over the timed steps."""
+        v = np.array([e[i].elapsed_time(e[i + 1]) * 1e3 / per_step for e in events])
+        return round(float(np.median(v)), 3), round(float(v.std() / v.mean()) if v.mean() > 0 else 0.0, 4)
+
+    ceiling = stream_ceiling(torch, dev, (N * K * q // 8 + 2 * N * K // g + 2 * K + 2 * N) // 16 * 16,
+                             args.layers, args.steps) if "gemv" in phases else None
+
     t_q = sum(e[0].elapsed_time(e[1]) for e in events) / 1e3   # seconds
     t_v = sum(e[1].elapsed_time(e[2]) for e in events) / 1e3
     t_b = sum(e[2].elapsed_time(e[3]) for e in events) / 1e3
@@ -537,6 +586,10 @@ def main() -> int:
                            "traffic": measured_traffic("gemv", args.mode),
                            "kernel": "gemv_kernel (ssq_matmul, M=1)",
                            "bytes_per_launch": gemv_bytes, "avg_launch_us": round(avg * 1e6, 3)}
+        out["roofline"]["median_launch_us"], out["roofline"]["cv"] = spread(1, args.layers)
+        if ceiling is not None:
+            ceiling["gemv_over_stream"] = round(gbs / ceiling["gbs"], 4)
+        out["ceiling_stream_read"] = ceiling
     if "batched" in phases:
         avg = t_b / n_gemv
         gbs = batched_bytes / avg / 1e9
@@ -547,6 +600,7 @@ def main() -> int:
                                    "kernel": f"skinny_split_kernel (ssq_matmul, M={args.batched_m})",
                                    "bytes_per_launch": batched_bytes, "avg_launch_us": round(avg * 1e6, 3),
                                    "tflops": round(2 * args.batched_m * N * K / avg / 1e12, 2)}
+        out["roofline_batched"]["median_launch_us"], out["roofline_batched"]["cv"] = spread(2, args.layers)
     if "gemm" in phases:
         avg = t_m / n_gemm
         tf = gemm_flops / avg / 1e12
@@ -557,6 +611,7 @@ def main() -> int:
                                 "traffic": measured_traffic("gemm", args.mode),
                                 "kernel": f"gemm_kernel (ssq_matmul, M={args.gemm_m})",
                                 "flops_per_launch": gemm_flops, "avg_launch_us": round(avg * 1e6, 3)}
+        out["roofline_gemm"]["median_launch_us"], out["roofline_gemm"]["cv"] = spread(3, args.gemm_layers)
     if "quantize" in phases:
         avg = t_q / args.steps
         gbs = quant_bytes / avg / 1e9
@@ -568,6 +623,7 @@ def main() -> int:
                                     "kernel": "quantize_kernel (ssq_quantize)",
                                     "bytes_per_launch": quant_bytes,
                                     "avg_launch_us": round(avg * 1e6, 3)}
+        out["roofline_quantize"]["median_launch_us"], out["roofline_quantize"]["cv"] = spread(0, 1)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w_bits, x1_bits, N, K, g, q, mode, gemv_bytes / N)
     out["host"] = platform.node()

@@ -17,6 +17,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libssq.so")
+# measurement-only kernels for bench.py (a streaming-read ceiling), not part of libssq
+BENCH_SRC = os.path.join(PKG, "csrc_bench")
+BENCH_LIB = os.path.join(PKG, "libssq_bench.so")
 
 ARCH = "gfx950"
 FLAGS = [
@@ -51,9 +54,21 @@ def _compile(src: str, build_dir: str, extra_flags: list[str]) -> str:
 def build(verbose: bool = False, lib_path: str = LIB, build_dir: str = BUILD,
           extra_flags: list[str] | None = None) -> str:
     """Compile every HIP source and link libssq.so (or lib_path); returns the library path.
-    extra_flags (e.g. -D tuning macros) go to every compile."""
+    extra_flags (e.g. -D tuning macros) go to every compile.  The default build also
+    links bench.py's measurement library (libssq_bench.so)."""
+    path = _link(sources(), lib_path, build_dir, extra_flags)
+    if verbose:
+        print(f"built {path}")
+    if lib_path == LIB:
+        bench_srcs = sorted(os.path.join(BENCH_SRC, f) for f in os.listdir(BENCH_SRC) if f.endswith(".hip"))
+        bpath = _link(bench_srcs, BENCH_LIB, os.path.join(build_dir, "bench"), [])
+        if verbose:
+            print(f"built {bpath}")
+    return path
+
+
+def _link(srcs: list[str], lib_path: str, build_dir: str, extra_flags: list[str] | None) -> str:
     os.makedirs(build_dir, exist_ok=True)
-    srcs = sources()
     with ThreadPoolExecutor(min(8, len(srcs))) as ex:
         objs = list(ex.map(lambda f: _compile(f, build_dir, extra_flags or []), srcs))
     tmp = lib_path + ".tmp"
@@ -62,8 +77,6 @@ def build(verbose: bool = False, lib_path: str = LIB, build_dir: str = BUILD,
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, lib_path)
-    if verbose:
-        print(f"built {lib_path}")
     return lib_path
 
 
