@@ -67,7 +67,16 @@ __device__ __forceinline__ void permute_x(const uint32_t (&X)[16], uint32_t (&xp
   }
 }
 
-// sum_{k in block} x[k] * (128 + u[k]) in fp32.  `magic` holds kMagic (in a VGPR).
+// q = 2 fields at mantissa bits 2-3 and 4-5 are OR-ed into the bf16 constants 32 and 8
+// instead of 128: with exponent 134 - 2c the field at bits 2c..2c+1 adds exactly u, so
+// the pair needs no shift.  The fields of a dword then fall into three offset classes
+// c (base 128, 32 or 8) by their position j in the dword's 8 pairs.
+constexpr uint32_t kMagicQ2[3] = {0x43004300u, 0x42004200u, 0x41004100u};
+constexpr float kBaseQ2[3] = {128.0f, 32.0f, 8.0f};
+constexpr int kClassQ2[8] = {0, 1, 2, 0, 0, 1, 2, 0};
+
+// sum_{k in block} x[k] * (base(k) + u[k]) in fp32, base 128 except for q = 2 (above).
+// `magic` holds kMagic (in a VGPR).
 template <int Q>
 __device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&xp)[16], uint32_t magic) {
   float acc = 0.0f;
@@ -81,11 +90,19 @@ __device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&x
       acc = dot2(and_or(w4 >> 8, 0x000F000Fu, magic), xp[4 * d + 3], acc);
     }
   } else if constexpr (Q == 2) {
+    // pair j of the dword holds fields (j, j + 8): bits 2j of each half-word
 #pragma unroll
-    for (int d = 0; d < 2; ++d)
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        acc = dot2(and_or(b.d[d] >> (2 * j), 0x00030003u, magic), xp[8 * d + j], acc);
+    for (int d = 0; d < 2; ++d) {
+      const uint32_t w = b.d[d], w6 = w >> 6, w8 = w >> 8, w14 = w >> 14;
+      acc = dot2(and_or(w, 0x00030003u, magic), xp[8 * d + 0], acc);
+      acc = dot2(and_or(w, 0x000C000Cu, kMagicQ2[1]), xp[8 * d + 1], acc);
+      acc = dot2(and_or(w, 0x00300030u, kMagicQ2[2]), xp[8 * d + 2], acc);
+      acc = dot2(and_or(w6, 0x00030003u, magic), xp[8 * d + 3], acc);
+      acc = dot2(and_or(w8, 0x00030003u, magic), xp[8 * d + 4], acc);
+      acc = dot2(and_or(w8, 0x000C000Cu, kMagicQ2[1]), xp[8 * d + 5], acc);
+      acc = dot2(and_or(w8, 0x00300030u, kMagicQ2[2]), xp[8 * d + 6], acc);
+      acc = dot2(and_or(w14, 0x00030003u, magic), xp[8 * d + 7], acc);
+    }
   } else {
     // Re-split the 96 bits into four 24-bit words of 8 fields, then move fields 4..7 of
     // each word up to bit 16 so that pairs (e_j, e_{j+4}) share one shift.
@@ -198,18 +215,32 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
 
   auto consume = [&](const uint32_t (&X)[16], const Block<Q> (&cb)[kRows], const uint32_t (&sbits)[kRows],
                      const uint32_t (&zbits)[kRows]) {
-    float xs = 0.0f;  // sum of the block's activations
-#pragma unroll
-    for (int i = 0; i < 16; ++i) xs = dot2(X[i], kOnes, xs);
     uint32_t xp[16];
     permute_x<Q>(X, xp);
+    // xs: sum of the block's activations; xb: sum of base(k) x[k], the constant part of
+    // block_dot (128 xs except for q = 2, whose pairs carry three bases)
+    float xs = 0.0f, xb;
+    if constexpr (Q == 2) {
+      float cs[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int i = 0; i < 16; ++i) cs[kClassQ2[i & 7]] = dot2(xp[i], kOnes, cs[kClassQ2[i & 7]]);
+      xs = cs[0] + cs[1] + cs[2];
+      xb = __builtin_fmaf(kBaseQ2[2], cs[2], __builtin_fmaf(kBaseQ2[1], cs[1], kBaseQ2[0] * cs[0]));
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) xs = dot2(X[i], kOnes, xs);
+      xb = kMagicValue * xs;
+    }
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
       const float acc = block_dot<Q>(cb[r], xp, magic);
       const float sc = f16_bits_to_f32(sbits[r]);
       if constexpr (META == kMetaMin) {    // s * sum x u + m * sum x
-        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-kMagicValue, xs, acc), yacc[r]);
+        yacc[r] = __builtin_fmaf(sc, acc - xb, yacc[r]);
         yacc[r] = __builtin_fmaf(f16_bits_to_f32(zbits[r]), xs, yacc[r]);
+      } else if constexpr (Q == 2) {
+        const float o = META == kMetaZp ? (float)zbits[r] : (float)(1 << (Q - 1));
+        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-o, xs, acc - xb), yacc[r]);
       } else {
         const float off = META == kMetaZp ? kMagicValue + (float)zbits[r] : kSymOffset;
         yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
