@@ -111,8 +111,9 @@ int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int 
  *   o = 2^(q-1) when zp == NULL (symmetric formats, signed or not: the sign
  *   lives in the scale, so both run the same kernel), o = zp[n, b] otherwise.
  * Products accumulate in fp32; y is rounded to bf16 (half to even).
- * M = 1 runs a streaming GEMV; 2 <= M <= 32 (batched decode) dequantizes each
- * weight once into bf16 MFMA operands shared by all tokens; larger M runs a tiled
+ * M = 1 and M = 2 run a streaming GEMV (two tokens share each unpacked block);
+ * 3 <= M <= 32 (batched decode) dequantizes each weight once into bf16 MFMA
+ * operands shared by all tokens; larger M runs a tiled
  * kernel that dequantizes weight tiles into LDS and multiplies them with bf16 MFMA.
  *
  *   x      device, bf16 bits [M, K] row-major, read only
@@ -134,9 +135,9 @@ int ssq_matmul(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_
  * ssq_matmul_workspace_size -- bytes of workspace that let ssq_matmul_ws split
  * the reduction of an M x N x K product across workgroups (App. B.3 sums over
  * blocks of K, so disjoint block ranges can be reduced separately and added).
- * Returns 0 when splitting would not help (M = 1, or enough output tiles
- * already) or the arguments are invalid.  2 <= M <= 32 sizes the batched-decode
- * kernel's split, larger M the tiled kernel's.
+ * Returns 0 when splitting would not help (M <= 2: the streaming GEMV, or enough
+ * output tiles already) or the arguments are invalid.  3 <= M <= 32 sizes the
+ * batched-decode kernel's split, larger M the tiled kernel's.
  */
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q);
 

@@ -118,6 +118,44 @@ __device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&x
   return acc;
 }
 
+// The 16 bf16 code pairs of a block in the order block_dot multiplies them (for
+// several tokens the pairs are formed once and dotted with each token's activations).
+template <int Q>
+__device__ __forceinline__ void block_pairs(const Block<Q>& b, uint32_t magic, uint32_t (&w)[16]) {
+  if constexpr (Q == 4) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const uint32_t w4 = b.d[d] >> 4;
+      w[4 * d] = and_or(b.d[d], 0x000F000Fu, magic);
+      w[4 * d + 1] = and_or(w4, 0x000F000Fu, magic);
+      w[4 * d + 2] = and_or(b.d[d] >> 8, 0x000F000Fu, magic);
+      w[4 * d + 3] = and_or(w4 >> 8, 0x000F000Fu, magic);
+    }
+  } else if constexpr (Q == 2) {
+#pragma unroll
+    for (int d = 0; d < 2; ++d) {
+      const uint32_t v = b.d[d], v6 = v >> 6, v8 = v >> 8, v14 = v >> 14;
+      w[8 * d + 0] = and_or(v, 0x00030003u, magic);
+      w[8 * d + 1] = and_or(v, 0x000C000Cu, kMagicQ2[1]);
+      w[8 * d + 2] = and_or(v, 0x00300030u, kMagicQ2[2]);
+      w[8 * d + 3] = and_or(v6, 0x00030003u, magic);
+      w[8 * d + 4] = and_or(v8, 0x00030003u, magic);
+      w[8 * d + 5] = and_or(v8, 0x000C000Cu, kMagicQ2[1]);
+      w[8 * d + 6] = and_or(v8, 0x00300030u, kMagicQ2[2]);
+      w[8 * d + 7] = and_or(v14, 0x00030003u, magic);
+    }
+  } else {
+    const uint32_t v[4] = {b.d[0], __builtin_amdgcn_alignbit(b.d[1], b.d[0], 24),
+                           __builtin_amdgcn_alignbit(b.d[2], b.d[1], 16), b.d[2] >> 8};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t sp = (v[i] & 0xFFFu) | ((v[i] << 4) & 0x0FFF0000u);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[4 * i + j] = and_or(sp >> (3 * j), 0x00070007u, magic);
+    }
+  }
+}
+
 // Work split.  A workgroup of T threads (T a whole number of wavefronts, at most 512)
 // owns kRows consecutive rows; wavefront w takes 64 consecutive blocks of each row per
 // pass (lane i block 64w + i), and passes repeat T blocks further on until the row
@@ -173,7 +211,9 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int Q, int G, int META, bool VS>
+// T tokens (1 or 2) share each unpacked block; token t's activations start at x + t*K
+// and its outputs at y + t*N.
+template <int Q, int G, int META, bool VS, int T = 1>
 __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restrict__ x,
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales,
@@ -185,8 +225,9 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
   const uint8_t* const zp = static_cast<const uint8_t*>(meta);
   constexpr int kBlocksPerGroup = S::kBlocksPerGroup;
   constexpr float kSymOffset = kMagicValue + (float)(1 << (Q - 1));
-  __shared__ float partial[kMaxWaves][kRows];
+  __shared__ float partial[kMaxWaves][kRows * T];
   extern __shared__ u32x4 stage[];
+  constexpr int kWaveChunks = T * kXChunks + S::kScaleChunks + S::kZpChunks;
 
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -197,8 +238,8 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
   const uint32_t row_bytes = (uint32_t)K * Q / 8;
   const uint32_t groups_per_row = (uint32_t)K / G;
   const uint32_t magic = kMagic;
-  u32x4* const xw = stage + wave * S::kWaveChunks;
-  const uint8_t* const sw = reinterpret_cast<const uint8_t*>(xw + kXChunks);
+  u32x4* const xw = stage + wave * kWaveChunks;
+  const uint8_t* const sw = reinterpret_cast<const uint8_t*>(xw + T * kXChunks);
   const uint8_t* const zw = sw + S::kScaleChunks * 16;
 
   const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + (int64_t)row0 * row_bytes, (uint32_t)rows_here * row_bytes);
@@ -207,43 +248,64 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
   const __amdgpu_buffer_rsrc_t rz =
       make_rsrc(ZP ? zp + (int64_t)row0 * groups_per_row * kMetaSize : zp,
                 ZP ? (uint32_t)rows_here * groups_per_row * kMetaSize : 0u);
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)T * K * 2);
 
-  float yacc[kRows];
+  float yacc[T][kRows];
 #pragma unroll
-  for (int r = 0; r < kRows; ++r) yacc[r] = 0.0f;
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) yacc[t][r] = 0.0f;
 
-  auto consume = [&](const uint32_t (&X)[16], const Block<Q> (&cb)[kRows], const uint32_t (&sbits)[kRows],
+  auto consume = [&](const uint32_t (&X)[T][16], const Block<Q> (&cb)[kRows], const uint32_t (&sbits)[kRows],
                      const uint32_t (&zbits)[kRows]) {
-    uint32_t xp[16];
-    permute_x<Q>(X, xp);
+    uint32_t xp[T][16];
     // xs: sum of the block's activations; xb: sum of base(k) x[k], the constant part of
     // block_dot (128 xs except for q = 2, whose pairs carry three bases)
-    float xs = 0.0f, xb;
-    if constexpr (Q == 2) {
-      float cs[3] = {0.0f, 0.0f, 0.0f};
+    float xs[T], xb[T];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) cs[kClassQ2[i & 7]] = dot2(xp[i], kOnes, cs[kClassQ2[i & 7]]);
-      xs = cs[0] + cs[1] + cs[2];
-      xb = __builtin_fmaf(kBaseQ2[2], cs[2], __builtin_fmaf(kBaseQ2[1], cs[1], kBaseQ2[0] * cs[0]));
-    } else {
+    for (int t = 0; t < T; ++t) {
+      permute_x<Q>(X[t], xp[t]);
+      xs[t] = 0.0f;
+      if constexpr (Q == 2) {
+        float cs[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int i = 0; i < 16; ++i) xs = dot2(X[i], kOnes, xs);
-      xb = kMagicValue * xs;
+        for (int i = 0; i < 16; ++i) cs[kClassQ2[i & 7]] = dot2(xp[t][i], kOnes, cs[kClassQ2[i & 7]]);
+        xs[t] = cs[0] + cs[1] + cs[2];
+        xb[t] = __builtin_fmaf(kBaseQ2[2], cs[2], __builtin_fmaf(kBaseQ2[1], cs[1], kBaseQ2[0] * cs[0]));
+      } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) xs[t] = dot2(X[t][i], kOnes, xs[t]);
+        xb[t] = kMagicValue * xs[t];
+      }
     }
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
-      const float acc = block_dot<Q>(cb[r], xp, magic);
-      const float sc = f16_bits_to_f32(sbits[r]);
-      if constexpr (META == kMetaMin) {    // s * sum x u + m * sum x
-        yacc[r] = __builtin_fmaf(sc, acc - xb, yacc[r]);
-        yacc[r] = __builtin_fmaf(f16_bits_to_f32(zbits[r]), xs, yacc[r]);
-      } else if constexpr (Q == 2) {
-        const float o = META == kMetaZp ? (float)zbits[r] : (float)(1 << (Q - 1));
-        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-o, xs, acc - xb), yacc[r]);
+      float acc[T];
+      if constexpr (T == 1) {
+        acc[0] = block_dot<Q>(cb[r], xp[0], magic);
       } else {
-        const float off = META == kMetaZp ? kMagicValue + (float)zbits[r] : kSymOffset;
-        yacc[r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), yacc[r]);
+        uint32_t w[16];
+        block_pairs<Q>(cb[r], magic, w);
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          acc[t] = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[t] = dot2(w[i], xp[t][i], acc[t]);
+        }
+      }
+      const float sc = f16_bits_to_f32(sbits[r]);
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        if constexpr (META == kMetaMin) {    // s * sum x u + m * sum x
+          yacc[t][r] = __builtin_fmaf(sc, acc[t] - xb[t], yacc[t][r]);
+          yacc[t][r] = __builtin_fmaf(f16_bits_to_f32(zbits[r]), xs[t], yacc[t][r]);
+        } else if constexpr (Q == 2) {
+          const float o = META == kMetaZp ? (float)zbits[r] : (float)(1 << (Q - 1));
+          yacc[t][r] = __builtin_fmaf(sc, __builtin_fmaf(-o, xs[t], acc[t] - xb[t]), yacc[t][r]);
+        } else {
+          const float off = META == kMetaZp ? kMagicValue + (float)zbits[r] : kSymOffset;
+          yacc[t][r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs[t], acc[t]), yacc[t][r]);
+        }
       }
     }
   };
@@ -253,9 +315,12 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
     const int j = jw + lane;
     const bool live = j < nblk;
     // Loads first: activations, scales (and zero points), then the codes of each row.
-    u32x4 xq[4];
+    u32x4 xq[T][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) xq[i] = __builtin_amdgcn_raw_buffer_load_b128(rx, jw * 64 + 1024 * i + 16 * lane, 0, 0);
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        xq[t][i] = __builtin_amdgcn_raw_buffer_load_b128(rx, t * K * 2 + jw * 64 + 1024 * i + 16 * lane, 0, 0);
     u32x4 sq = {0, 0, 0, 0}, zq = {0, 0, 0, 0};
     uint32_t sbits[kRows], zbits[kRows];
     if constexpr (VS) {
@@ -289,18 +354,22 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
     // Through LDS: chunk c = 64 i + lane of the pass is piece c % 4 of block c / 4.
     wave_sync_lds();   // the previous pass's reads are done
 #pragma unroll
-    for (int i = 0; i < 4; ++i) xw[x_slot(16 * i + (lane >> 2), lane & 3)] = xq[i];
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xw[t * kXChunks + x_slot(16 * i + (lane >> 2), lane & 3)] = xq[t][i];
     if constexpr (VS) {
-      if (lane < S::kScaleChunks) xw[kXChunks + lane] = sq;
-      if constexpr (ZP) if (lane < S::kZpChunks) xw[kXChunks + S::kScaleChunks + lane] = zq;
+      if (lane < S::kScaleChunks) xw[T * kXChunks + lane] = sq;
+      if constexpr (ZP) if (lane < S::kZpChunks) xw[T * kXChunks + S::kScaleChunks + lane] = zq;
     }
     wave_sync_lds();
-    uint32_t X[16];
+    uint32_t X[T][16];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const u32x4 v = xw[x_slot(lane, p)];
-      X[4 * p] = v.x; X[4 * p + 1] = v.y; X[4 * p + 2] = v.z; X[4 * p + 3] = v.w;
-    }
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const u32x4 v = xw[t * kXChunks + x_slot(lane, p)];
+        X[t][4 * p] = v.x; X[t][4 * p + 1] = v.y; X[t][4 * p + 2] = v.z; X[t][4 * p + 3] = v.w;
+      }
     if constexpr (VS) {
       const int g = lane / kBlocksPerGroup;
 #pragma unroll
@@ -318,9 +387,10 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
   // four values of a lane into one, leaving in 16-lane row R the partials of row
   // (R & 1) * 2 + (R >> 1); four DPP steps then finish each 16-lane row.
   static_assert(kRows == 4, "the folded reduction handles four rows");
-  {
-    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[0]), __float_as_uint(yacc[1]), false, false);
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[2]), __float_as_uint(yacc[3]), false, false);
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[t][0]), __float_as_uint(yacc[t][1]), false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[t][2]), __float_as_uint(yacc[t][3]), false, false);
     const float s01 = __uint_as_float(a[0]) + __uint_as_float(a[1]);
     const float s23 = __uint_as_float(b[0]) + __uint_as_float(b[1]);
     const auto c = __builtin_amdgcn_permlane16_swap(__float_as_uint(s01), __float_as_uint(s23), false, false);
@@ -329,14 +399,24 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
     v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2,3,0,1]
     v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
     v = dpp_add<0x140, 0xF>(v);   // row_mirror
-    if ((lane & 15) == 0) partial[wave][((lane >> 4) & 1) * 2 + (lane >> 5)] = v;
+    if ((lane & 15) == 0) partial[wave][t * kRows + ((lane >> 4) & 1) * 2 + (lane >> 5)] = v;
   }
   __syncthreads();
-  if ((int)threadIdx.x < rows_here) {
-    const int waves = threads >> 6;
-    float v = 0.0f;
-    for (int w = 0; w < waves; ++w) v += partial[w][threadIdx.x];
-    y[row0 + threadIdx.x] = f32_to_bf16_bits(v);
+  if constexpr (T == 1) {
+    if ((int)threadIdx.x < rows_here) {
+      const int waves = threads >> 6;
+      float v = 0.0f;
+      for (int w = 0; w < waves; ++w) v += partial[w][threadIdx.x];
+      y[row0 + threadIdx.x] = f32_to_bf16_bits(v);
+    }
+  } else if ((int)threadIdx.x < kRows * T) {
+    const int t = (int)threadIdx.x / kRows, r = (int)threadIdx.x % kRows;
+    if (r < rows_here) {
+      const int waves = threads >> 6;
+      float v = 0.0f;
+      for (int w = 0; w < waves; ++w) v += partial[w][t * kRows + r];
+      y[(int64_t)t * N + row0 + r] = f32_to_bf16_bits(v);
+    }
   }
 }
 
@@ -388,7 +468,7 @@ __global__ __launch_bounds__(256) void matmul_f32_kernel(const float* __restrict
   }
 }
 
-template <int Q, int G, int META>
+template <int Q, int G, int META, int T = 1>
 hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
                          const void* meta, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
   using S = Stage<G, META>;
@@ -396,7 +476,7 @@ hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t
   const int64_t passes = (nblk + kMaxTeam - 1) / kMaxTeam;
   const int threads = (int)(((nblk + passes - 1) / passes + 63) / 64 * 64);
   const dim3 grid((unsigned)((N + kRows - 1) / kRows));
-  const size_t lds = (size_t)(threads / 64) * S::kWaveBytes;
+  const size_t lds = (size_t)(threads / 64) * (T * kXChunks + S::kScaleChunks + S::kZpChunks) * 16;
   // One load per wavefront covers the rows' scales (and zero points or minimums) when
   // every row's run of them starts 16-byte aligned.
   const int64_t groups = K / G;
@@ -404,9 +484,9 @@ hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t
                   (S::kMetaSize == 0 ||
                    (reinterpret_cast<uintptr_t>(meta) % 16 == 0 && (groups * S::kMetaSize) % 16 == 0));
   if (vs)
-    gemv_kernel<Q, G, META, true><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
+    gemv_kernel<Q, G, META, true, T><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
   else
-    gemv_kernel<Q, G, META, false><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
+    gemv_kernel<Q, G, META, false, T><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
   return hipGetLastError();
 }
 
@@ -424,6 +504,19 @@ hipError_t launch_gemv_bf16(const uint16_t* x, const uint8_t* codes, const uint1
                             GroupMeta meta, int64_t N, int64_t K, int group, int q, uint16_t* y,
                             hipStream_t stream) {
   SSQ_DISPATCH_QGM(gemv_dispatch, q, group, meta.kind, x, codes, scales, meta.ptr, N, K, y, stream);
+}
+
+// Two tokens through one pass over the weights (M = 2).
+template <int Q, int G, int META>
+hipError_t gemv2_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
+                          const void* meta, int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+  return gemv_dispatch<Q, G, META, 2>(x, codes, scales, meta, N, K, y, stream);
+}
+
+hipError_t launch_gemv2_bf16(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
+                             GroupMeta meta, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                             hipStream_t stream) {
+  SSQ_DISPATCH_QGM(gemv2_dispatch, q, group, meta.kind, x, codes, scales, meta.ptr, N, K, y, stream);
 }
 
 hipError_t launch_matmul_f32(const float* x, int64_t M, const uint8_t* codes,

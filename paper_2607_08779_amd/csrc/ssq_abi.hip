@@ -6,6 +6,12 @@
 
 #include "ssq_internal.h"
 
+namespace ssq {
+// Decode GEMV for two tokens (gemv.hip): each unpacked block serves both.
+hipError_t launch_gemv2_bf16(const uint16_t* x, const uint8_t* codes, const uint16_t* scales, GroupMeta meta,
+                             int64_t N, int64_t K, int group, int q, uint16_t* y, hipStream_t stream);
+}  // namespace ssq
+
 namespace {
 
 constexpr int64_t kMaxElems = int64_t(1) << 40;   // rows*cols or N*K
@@ -65,12 +71,13 @@ int check_diagnostics(const void* W, int64_t rows, int64_t cols, int group, int 
 ssq::GroupMeta zero_points(const uint8_t* zp) { return {zp, zp ? ssq::kMetaZp : ssq::kMetaNone}; }
 ssq::GroupMeta minimums(const uint16_t* mins) { return {mins, ssq::kMetaMin}; }
 
-// bf16 matmul kernel choice by token count: streaming GEMV (M = 1), skinny-M MFMA
+// bf16 matmul kernel choice by token count: streaming GEMV (M = 1, 2), skinny-M MFMA
 // kernel (batched decode), tiled MFMA GEMM with an optional split reduction (prefill).
 int dispatch_bf16(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                   ssq::GroupMeta meta, int64_t N, int64_t K, int group, int q, uint16_t* y,
                   void* workspace, size_t workspace_bytes, hipStream_t stream) {
   if (M == 1) return status_of(ssq::launch_gemv_bf16(x, codes, scales, meta, N, K, group, q, y, stream));
+  if (M == 2) return status_of(ssq::launch_gemv2_bf16(x, codes, scales, meta, N, K, group, q, y, stream));
   if (M <= ssq::kSkinnyMaxM)
     return status_of(ssq::launch_skinny_bf16(x, M, codes, scales, meta, N, K, group, q, y, workspace,
                                              workspace_bytes, stream));
@@ -155,7 +162,7 @@ int ssq_matmul_min(const uint16_t* x, int64_t M, const uint8_t* codes, const uin
 }
 
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q) {
-  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M < 2 || N == 0) return 0;
+  if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M <= 2 || N == 0) return 0;   // GEMV: no split
   return M <= ssq::kSkinnyMaxM ? ssq::skinny_workspace_bytes(M, N, K) : ssq::gemm_workspace_bytes(M, N, K);
 }
 

@@ -195,7 +195,7 @@ def test_skinny_split_reduction_ragged(q, mode):
     check_matmul(w, x, 32, q, mode, tag="skinny split 7x200x3104", workspace=True, repeat=3)
 
 
-@pytest.mark.parametrize("M", [2, 16, 17, 32])
+@pytest.mark.parametrize("M", [3, 16, 17, 32])
 @pytest.mark.parametrize("group", [32, 128])
 def test_skinny_split_token_counts(M, group):
     w = rand_w(300, 8192, seed=M + group)
@@ -352,3 +352,13 @@ def test_llama3_70b_matmul_full_size(M, workspace):
         x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
         check_matmul(w, x, 32, 2, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=24, seed=M),
                      tag=f"70b {name} M={M}", workspace=workspace, repeat=2 if workspace else 1)
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 128])
+@pytest.mark.parametrize("mode", MODES)
+def test_gemv_two_tokens_all_formats(q, group, mode):
+    # M = 2 takes the two-token GEMV: 37 rows (ragged row groups), K = 19200 (two passes)
+    w = rand_w(37, 19200, seed=q * 7 + group + mode)
+    x = synth.activations(2, 19200, seed=q + group)
+    check_matmul(w, x, group, q, mode, tag=f"gemv M=2 q={q} g={group} m={mode}")
