@@ -362,3 +362,13 @@ def test_gemv_two_tokens_all_formats(q, group, mode):
     w = rand_w(37, 19200, seed=q * 7 + group + mode)
     x = synth.activations(2, 19200, seed=q + group)
     check_matmul(w, x, group, q, mode, tag=f"gemv M=2 q={q} g={group} m={mode}")
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_gemv_two_tokens_full_size(mode):
+    # 4096x14336 at M = 2: seven wavefronts each staging two tokens' activations plus
+    # the scales and metadata (the largest LDS of the GEMV), sampled rows
+    spec = synth.llama3_8b_decode().layers["down_proj"]
+    w = weights_host(spec)
+    x = synth.activations(2, spec.cols, seed=77)
+    check_matmul(w, x, 32, 4, mode, rows_idx=sample_rows(spec.rows, 48, seed=mode), tag=f"gemv M=2 full m={mode}")
