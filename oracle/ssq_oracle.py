@@ -51,7 +51,7 @@ MODE_NAMES = {SIGNED_SYM: "signed_sym", UNSIGNED_SYM: "unsigned_sym", ASYM: "asy
               ASYM_MIN: "asym_min"}
 
 READINGS = {
-    "tie_break": "Eq. (5) asks for deterministic tie-breaking in argmax|w_i|; when both +M and -M "
+    "tie_break": "Eq. (5) breaks ties in argmax|w_i| by an unnamed fixed rule; when both +M and -M "
                  "occur the oracle takes gamma=+1 (gamma=-1 only if max(w) > -min(w) strictly).",
     "rounding": "The round-to-nearest operator of Eq. (1) resolves exact halves to even.",
     "division": "t = w/s is one IEEE binary32 division, correctly rounded, then rounded to an integer.",
