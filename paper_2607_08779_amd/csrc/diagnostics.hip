@@ -41,29 +41,28 @@ constexpr int kLineWords = 64;
 __device__ unsigned int g_block_counts[9 * kMaxBlocks];
 __device__ unsigned int g_arrivals[(kClasses + 1) * kLineWords];
 
-// This lane's 8 weights of chunk `c` of the trip whose first chunk the buffer resource
-// starts at; a chunk past the end reads as zeros (the load is out of the resource's
-// range), so every lane runs the same code.
+// Dwords per chunk of 8 weights: 4 (bf16 pairs) or 8 (binary32).
 template <typename In>
-__device__ __forceinline__ void load_chunk(__amdgpu_buffer_rsrc_t r, uint32_t c, bool valid, float (&w)[8]) {
+constexpr int kWords = 4 * (int)sizeof(In) / 2;
+
+// This lane's 8 weights of chunk `c` of the trip whose first chunk the buffer resource
+// starts at, as loaded; a chunk past the end reads as zeros (the resource ends at the
+// matrix, so the load is out of its range), and every lane runs the same code.
+template <typename In>
+__device__ __forceinline__ void load_chunk(__amdgpu_buffer_rsrc_t r, uint32_t c, uint32_t (&d)[kWords<In>]) {
   constexpr uint32_t kBytes = 8 * sizeof(In);
-  const int off = valid ? (int)(c * kBytes) : (int)0x80000000;
-  if constexpr (sizeof(In) == 2) {
-    const u32x4 d = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kStream);
-    w[0] = bf16_lo(d.x); w[1] = bf16_hi(d.x); w[2] = bf16_lo(d.y); w[3] = bf16_hi(d.y);
-    w[4] = bf16_lo(d.z); w[5] = bf16_hi(d.z); w[6] = bf16_lo(d.w); w[7] = bf16_hi(d.w);
-  } else {
-    const u32x4 a = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kStream);
-    const u32x4 b = __builtin_amdgcn_raw_buffer_load_b128(r, off, 16, kStream);
-    w[0] = __uint_as_float(a.x); w[1] = __uint_as_float(a.y); w[2] = __uint_as_float(a.z);
-    w[3] = __uint_as_float(a.w); w[4] = __uint_as_float(b.x); w[5] = __uint_as_float(b.y);
-    w[6] = __uint_as_float(b.z); w[7] = __uint_as_float(b.w);
+  const int off = (int)(c * kBytes);
+#pragma unroll
+  for (int h = 0; h < kWords<In> / 4; ++h) {
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 16 * h, kStream);
+    d[4 * h] = v.x; d[4 * h + 1] = v.y; d[4 * h + 2] = v.z; d[4 * h + 3] = v.w;
   }
 }
 
-// One group's statistics from this lane's 8 weights; valid in every lane of the group.
+// One group's statistics from its weights as binary32 values (every lane of the
+// wavefront calls this: DPP exchanges).
 template <int Q, int G>
-__device__ __forceinline__ void group_stats(const float (&w)[8], int& m, double& g) {
+__device__ __forceinline__ void group_stats_f32(const float (&w)[8], int& m, double& g) {
   constexpr int kLanes = G / 8;
   float mx = w[0], mn = w[0];
 #pragma unroll
@@ -71,6 +70,31 @@ __device__ __forceinline__ void group_stats(const float (&w)[8], int& m, double&
   mx = group_max<kLanes>(mx);
   const float nmn = group_max<kLanes>(-mn);
   sign_stats<Q, G>(w, mx, nmn, m, g);
+}
+
+// One group's statistics from this lane's 8 weights as loaded; valid in every lane of
+// the group.  bf16 weights take the packed 16-bit arithmetic unless a group of the
+// wavefront has a tiny or zero maximum (the choice is uniform over the wavefront: both
+// paths exchange values between lanes).
+template <typename In, int Q, int G>
+__device__ __forceinline__ void group_stats(const uint32_t (&d)[kWords<In>], int& m, double& g) {
+  if constexpr (sizeof(In) == 2) {
+    bool gamma_neg;
+    const uint32_t mb = group_absmax_bf16<G>(d, gamma_neg);
+    if (__builtin_amdgcn_ballot_w64(mb < 0x100u) == 0) {
+      sign_stats_bf16<Q, G>(d, mb, gamma_neg, m, g);
+    } else {
+      float w[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) { w[2 * j] = bf16_lo(d[j]); w[2 * j + 1] = bf16_hi(d[j]); }
+      group_stats_f32<Q, G>(w, m, g);
+    }
+  } else {
+    float w[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = __uint_as_float(d[i]);
+    group_stats_f32<Q, G>(w, m, g);
+  }
 }
 
 template <typename In, int Q, int G>
@@ -83,33 +107,74 @@ __global__ __launch_bounds__(kThreads, 8) void diagnostics_kernel(const In* __re
   const bool leader = threadIdx.x % kLanes == 0;
   uint32_t packed[5] = {0, 0, 0, 0, 0};   // cell k = 3 (sign m + 1) + (sign g + 1): field k % 2 of word k / 2
   const int64_t stride = (int64_t)gridDim.x * (kThreads * kUnroll);
-  // total_chunks is a multiple of G/8, so a group's lanes are all valid or all not.
-  for (int64_t base = (int64_t)blockIdx.x * (kThreads * kUnroll); base < total_chunks; base += stride) {
-    const int64_t left = total_chunks - base;             // > 0
-    const uint32_t span = (uint32_t)std::min<int64_t>(left, kThreads * kUnroll) * (8 * sizeof(In));
-    const __amdgpu_buffer_rsrc_t r = make_rsrc(W + 8 * base, span);
-    float w[kUnroll][8];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const uint32_t c = u * kThreads + threadIdx.x;
-      load_chunk<In>(r, c, base + c < total_chunks, w[u]);
-    }
+  // The statistics of one trip's chunks, and the tally.  total_chunks is a multiple of
+  // G/8, so a group's lanes are all valid or all not.
+  // Margins and gains go out through buffer stores that every lane issues: a lane other
+  // than its group's leader, and a group past the end of the matrix, store out of the
+  // resource's range (discarded).  Unconditional stores keep the memory counter exact,
+  // so the waits for the next trip's loads do not also wait for these stores.
+  // byte offsets of this lane's group within a trip's first part (0x80000000 and above:
+  // out of range)
+  const uint32_t off_m = leader ? 2u * (threadIdx.x / kLanes) : 0x80000000u;
+  const uint32_t off_g = leader ? 4u * (threadIdx.x / kLanes) : 0x80000000u;
+  auto consume = [&](int64_t base, uint32_t (&w)[kUnroll][kWords<In>]) {
+    const int64_t g0 = base / kLanes;                                       // base is a multiple of G/8
+    const int64_t groups_left = (total_chunks - base) / kLanes;             // > 0
+    const uint32_t ng = (uint32_t)std::min<int64_t>(groups_left, kThreads * kUnroll / kLanes);
+    const __amdgpu_buffer_rsrc_t rm = make_rsrc(margin + g0, ng * 2);
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(gain + g0, ng * 4);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t chunk = base + u * kThreads + threadIdx.x;
       int m;
       double g;
-      group_stats<Q, G>(w[u], m, g);
-      if (leader && chunk < total_chunks) {
-        const int64_t group = chunk / kLanes;
-        const float gf = (float)g;
-        margin[group] = (int16_t)m;
-        gain[group] = gf;
-        const int k = ((m > 0) - (m < 0) + 1) * 3 + ((gf > 0.0f) - (gf < 0.0f) + 1);
-        const uint32_t inc = (k & 1) ? 0x10000u : 1u;
+      group_stats<In, Q, G>(w[u], m, g);
+      const float gf = (float)g;
+      constexpr uint32_t kPart = kThreads / kLanes;                          // groups per trip part
+      __builtin_amdgcn_raw_buffer_store_b16((unsigned short)m, rm, (int)(off_m + 2 * u * kPart), 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(gf), rg, (int)(off_g + 4 * u * kPart), 0, 0);
+      const int k = ((m > 0) - (m < 0) + 1) * 3 + ((gf > 0.0f) - (gf < 0.0f) + 1);
+      const uint32_t inc = (leader && chunk < total_chunks) ? ((k & 1) ? 0x10000u : 1u) : 0u;
 #pragma unroll
-        for (int j = 0; j < 5; ++j) packed[j] += (k >> 1) == j ? inc : 0u;
-      }
+      for (int j = 0; j < 5; ++j) packed[j] += (k >> 1) == j ? inc : 0u;
+    }
+  };
+  // This lane's chunks of the trip starting at `base` (zeros past the end of the matrix,
+  // and for a trip that starts past it: the resource then covers no bytes).
+  auto load_trip = [&](int64_t base, uint32_t (&w)[kUnroll][kWords<In>]) {
+    const int64_t left = total_chunks - base;
+    const uint32_t span = left > 0 ? (uint32_t)std::min<int64_t>(left, kThreads * kUnroll) * (8 * sizeof(In)) : 0u;
+    const __amdgpu_buffer_rsrc_t r = make_rsrc(left > 0 ? W + 8 * base : W, span);
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const uint32_t c = u * kThreads + threadIdx.x;
+      load_chunk<In>(r, c, w[u]);
+    }
+  };
+  int64_t base = (int64_t)blockIdx.x * (kThreads * kUnroll);
+  if constexpr (sizeof(In) == 2) {
+    // bf16: the next trip's loads are in flight while this trip's statistics run, so a
+    // wavefront waits on memory once rather than once per trip.
+    // Two register sets alternate roles (a copy between them would wait for the loads).
+    uint32_t a[kUnroll][kWords<In>], b[kUnroll][kWords<In>];
+    load_trip(base, a);
+    while (base < total_chunks) {
+      load_trip(base + stride, b);
+      __builtin_amdgcn_sched_barrier(0);
+      consume(base, a);
+      base += stride;
+      if (base >= total_chunks) break;
+      load_trip(base + stride, a);
+      __builtin_amdgcn_sched_barrier(0);
+      consume(base, b);
+      base += stride;
+    }
+  } else {
+    for (; base < total_chunks; base += stride) {
+      uint32_t w[kUnroll][kWords<In>];
+      load_trip(base, w);
+      __builtin_amdgcn_sched_barrier(0);      // every load of the trip is in flight before any arithmetic
+      consume(base, w);
     }
   }
   if (tally == nullptr) return;                          // uniform over the grid

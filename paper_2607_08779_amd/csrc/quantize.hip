@@ -107,7 +107,17 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(const In* __restrict
     const float nmn = group_max<kLanesPerGroup>(-mn);  // -min_j w_j
     int diag_m = 0;
     double diag_g = 0.0;
-    if constexpr (DIAG) sign_stats<Q, G>(w[u], mx, nmn, diag_m, diag_g);
+    if constexpr (DIAG) {
+      // bf16 weights: packed 16-bit statistics unless a group of the wavefront has a
+      // tiny or zero maximum (a wave-uniform choice: both exchange values between lanes)
+      const uint32_t mb = (__float_as_uint(fmaxf(mx, nmn)) >> 16) & 0x7FFFu;
+      if (sizeof(In) == 2 && __builtin_amdgcn_ballot_w64(mb < 0x100u) == 0) {
+        uint32_t d[4];
+        bf16_pairs_perm(w[u], d);
+        sign_stats_bf16<Q, G>(d, mb, mx > nmn, diag_m, diag_g);
+      } else
+        sign_stats<Q, G>(w[u], mx, nmn, diag_m, diag_g);
+    }
 
     uint32_t packed = 0;
     uint16_t scale_bits = 0;

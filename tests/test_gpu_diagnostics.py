@@ -66,6 +66,58 @@ def test_diagnostics_edge_groups():
         check(w, True, 32, q, tag=f"edge q={q}")
 
 
+def packed_edge_rows(rng):
+    """512-weight rows (one wavefront's span in both kernels) of groups that stress the
+    bf16 integer statistics: weights exactly at each T = M (1 - 2^-q) and one ulp above,
+    +M/-M ties, constant groups, huge values, maxima at the smallest exponents the
+    integer path takes, a wave whose groups mix a tiny maximum (the binary32 path) with
+    ordinary ones, signed zeros, one-sided groups."""
+    rows = []
+    r = rng.standard_normal(512) * 0.05
+    for k, q in enumerate((2, 3, 4)):
+        T = 1.0 - 2.0 ** -q
+        for j, v in enumerate((T, T + 2 ** -8, -T, -(T + 2 ** -8))):
+            g0 = 32 * (4 * k + j)
+            r[g0] = 1.0 if j % 2 == 0 else -1.0
+            r[g0 + 1: g0 + 6] = v
+    rows.append(r)
+    t = rng.standard_normal(512) * 0.1
+    t[::32] = 1.0; t[1::32] = -1.0; t[2::64] = -1.0
+    rows.append(t)
+    c = np.full(512, 0.375); c[256:] = -0.8125
+    rows.append(c)
+    rows.append(rng.standard_normal(512) * 1e35)
+    e2 = rng.uniform(-1.9, 1.9, 512) * 2.0 ** -125        # maxima with biased exponent 2
+    e2[::32] = 1.5 * 2.0 ** -125
+    rows.append(e2)
+    mixed = rng.standard_normal(512) * 0.02
+    mixed[128:256] = rng.choice([-1.0, 1.0], 128) * rng.uniform(1, 1.99, 128) * 2.0 ** -126   # exponent 1
+    rows.append(mixed)
+    z = rng.standard_normal(512) * 0.02
+    z[0:32] = -0.0; z[0] = 0.5                          # -0 beside a positive maximum
+    z[32:64] = -np.abs(z[32:64])                       # all negative
+    z[64:96] = 0.0; z[70] = -0.25                      # a single nonzero
+    z[96:128] = np.abs(z[96:128])                      # all positive
+    rows.append(z)
+    cx = np.zeros(512); cx[::32] = 1.0; cx[1::32] = 0.76; cx[2::32] = 0.76; cx[3::32] = -0.99; cx[4::32] = -0.99
+    cx[5::32] = 0.01
+    rows.append(cx)
+    return synth.to_bf16_bits(np.stack(rows).astype(np.float32))
+
+
+@pytest.mark.parametrize("group", [32, 64, 128])
+def test_diagnostics_bf16_packed_edges(group):
+    w = packed_edge_rows(np.random.default_rng(group))
+    for q in (2, 3, 4):
+        check(w, True, group, q, tag=f"packed edges g={group} q={q}")
+        codes, scales, margin, gain = ssq.ssq_quantize_diag(to_device(w, True), group, q)
+        torch.cuda.synchronize()
+        with np.errstate(over="ignore"):
+            d = O.sign_diagnostics(widen(w, True), group, q)
+        assert np.array_equal(margin.cpu().numpy(), d.margin), f"fused g={group} q={q}: margins"
+        assert np.array_equal(gain.cpu().numpy(), d.gain), f"fused g={group} q={q}: gains"
+
+
 def test_diagnostics_llama3_8b_down_proj_full_size():
     """4096x14336 at q in {2,3,4}: sampled rows bit for bit; tally consistent with the
     full per-group outputs (the GPU tally counts what the GPU stored)."""
