@@ -26,6 +26,9 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",
     "-ffp-contract=off",                      # every fma in the kernels is written out
     "-mllvm", "-amdgpu-mfma-vgpr-form=1",     # MFMA accumulators in VGPRs: no AGPR copies in loops
+    # the first kernel arguments arrive in SGPRs at dispatch (no scalar load before the
+    # first address is known; ~0.2 us per decode GEMV launch)
+    "-mllvm", "-amdgpu-kernarg-preload-count=16",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}",
 ]

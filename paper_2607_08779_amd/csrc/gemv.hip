@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
                                                         const uint8_t* __restrict__ codes,
                                                         const uint16_t* __restrict__ scales,
                                                         const void* __restrict__ meta, int N, int K,
-                                                        uint16_t* __restrict__ y) {
+                                                        uint16_t* __restrict__ y, int threads) {
   using S = Stage<G, META>;
   constexpr bool ZP = META != kMetaNone;                   // any per-group metadata
   constexpr int kMetaSize = S::kMetaSize;
@@ -231,7 +231,6 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
 
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int threads = blockDim.x;
   const int row0 = (int)blockIdx.x * kRows;
   const int rows_here = N - row0 < kRows ? N - row0 : kRows;   // >= 1
   const int nblk = K / 32;
@@ -484,9 +483,11 @@ hipError_t gemv_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t
                   (S::kMetaSize == 0 ||
                    (reinterpret_cast<uintptr_t>(meta) % 16 == 0 && (groups * S::kMetaSize) % 16 == 0));
   if (vs)
-    gemv_kernel<Q, G, META, true, T><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
+    gemv_kernel<Q, G, META, true, T><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y,
+                                                                     threads);
   else
-    gemv_kernel<Q, G, META, false, T><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y);
+    gemv_kernel<Q, G, META, false, T><<<grid, threads, lds, stream>>>(x, codes, scales, meta, (int)N, (int)K, y,
+                                                                      threads);
   return hipGetLastError();
 }
 
