@@ -33,6 +33,9 @@
  *   - Every pointer is a device pointer owned by the caller.  The library
  *     allocates nothing, frees nothing and keeps no pointer after returning;
  *     scratch memory, where a path can use it, is a caller-provided workspace.
+ *     The one exception is a static device array (about 90 KB per GPU, held
+ *     until the process ends) in which ssq_sign_diagnostics meets its blocks
+ *     to form the tally.
  *   - W, x, y and codes must be 16-byte aligned; scales and mins 2-byte aligned.
  *   - bf16 and fp16 tensors are passed as their uint16_t bit patterns.
  *   - Inputs must be finite; NaN/Inf inputs give unspecified codes.
