@@ -74,3 +74,38 @@ def test_diagnostics_at_max_k():
     assert np.array_equal(margin.cpu().numpy(), d.margin)
     assert np.array_equal(gain.cpu().numpy(), d.gain)
     assert np.array_equal(tally.cpu().numpy(), d.tally)
+
+
+def test_large_row_count():
+    """Two million and three weight rows (K = 64): grids of 2^19 GEMV workgroups and 2^14
+    batched-decode and GEMM row blocks, ragged at the end.  Quantize, the GEMV at M = 1
+    and 2, batched decode (M = 16) and the GEMM (M = 40) with their workspaces, and the
+    sign-rule diagnostics, each against the oracle on sampled rows (the last ones
+    included); the tally against the counts of the full outputs."""
+    N, K, group, q = (1 << 21) + 3, 64, 32, 4
+    rng = np.random.default_rng(11)
+    wb = synth.to_bf16_bits(rng.standard_normal((N, K), dtype=np.float32) * np.float32(0.02))
+    W = to_device(wb, True)
+    rows = np.unique(np.concatenate([rng.choice(N, 61, replace=False), np.arange(N - 3, N)]))
+    wf = O.bf16_bits_to_f32(wb[rows])
+    codes, scales, zp = ssq.ssq_quantize(W, group, q, O.SIGNED_SYM)
+    torch.cuda.synchronize()
+    r = O.quantize(wf, group, q, O.SIGNED_SYM)
+    assert np.array_equal(codes.cpu().numpy()[rows], r.codes)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint16)[rows], r.scales)
+    for M in (1, 2, 16, 40):
+        x = synth.activations(M, K, seed=M)
+        ws = ssq.ssq_matmul_workspace(M, N, K, group, q)
+        y = ssq.ssq_matmul(to_device(x, True), codes, scales, zp, N, K, group, q, workspace=ws)
+        ref = O.matmul(O.bf16_bits_to_f32(x), r.codes, r.scales, None, len(rows), K, group, q)
+        err = rel_l2(y_to_f64(y)[:, rows], ref)
+        log_metric(test="limits", tag=f"N=2^21+3 M={M}", rel_l2=err)
+        assert err <= 2e-2, f"M={M}: rel L2 {err:.2e}"
+    margin, gain, tally = ssq.ssq_sign_diagnostics(W, group, q)
+    torch.cuda.synchronize()
+    d = O.sign_diagnostics(wf, group, q)
+    m, g = margin.cpu().numpy(), gain.cpu().numpy()
+    assert np.array_equal(m[rows], d.margin) and np.array_equal(g[rows], d.gain)
+    counts = np.zeros((3, 3), np.int64)
+    np.add.at(counts, (np.sign(m).astype(np.int64) + 1, np.sign(g).astype(np.int64) + 1), 1)
+    assert np.array_equal(tally.cpu().numpy(), counts)
