@@ -156,7 +156,7 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_q8_kernel(const int8_t* __restr
                                                            const uint8_t* __restrict__ codes,
                                                            const uint16_t* __restrict__ scales,
                                                            const void* __restrict__ meta, int N, int K,
-                                                           uint16_t* __restrict__ y, int64_t token0) {
+                                                           int threads, int token0, uint16_t* __restrict__ y) {
   constexpr int kBlocksPerGroup = G / 32;
   constexpr int kMetaSize = META == kMetaZp ? 1 : META == kMetaMin ? 2 : 0;
   __shared__ float partial[kMaxWaves][kRows];
@@ -164,7 +164,6 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_q8_kernel(const int8_t* __restr
   const int64_t m = token0 + blockIdx.y;
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int threads = blockDim.x;
   const int row0 = (int)blockIdx.x * kRows;
   const int rows_here = N - row0 < kRows ? N - row0 : kRows;   // >= 1
   const int nblk = K / 32;
@@ -264,7 +263,8 @@ hipError_t gemv_q8_dispatch(const int8_t* qx, const uint16_t* dx, int64_t M, con
   constexpr int64_t kMaxGridY = 65535;
   for (int64_t m0 = 0; m0 < M; m0 += kMaxGridY) {
     const dim3 grid((unsigned)((N + kRows - 1) / kRows), (unsigned)std::min<int64_t>(M - m0, kMaxGridY));
-    gemv_q8_kernel<Q, G, META><<<grid, threads, 0, stream>>>(qx, dx, codes, scales, meta, (int)N, (int)K, y, m0);
+    gemv_q8_kernel<Q, G, META><<<grid, threads, 0, stream>>>(qx, dx, codes, scales, meta, (int)N, (int)K,
+                                                             threads, (int)m0, y);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
