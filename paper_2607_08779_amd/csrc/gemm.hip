@@ -106,10 +106,9 @@ Plan plan_for(int64_t M, int64_t N, int64_t K) {
 
 template <int Q, int G, int META, int WM>
 __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
-    const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales, const void* __restrict__ meta, int N, int K,
-    uint16_t* __restrict__ y, int splits, float* __restrict__ partials,
-    unsigned int* __restrict__ counters) {
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const void* __restrict__ meta, int M, int N, int K, int splits, uint16_t* __restrict__ y,
+    float* __restrict__ partials, unsigned int* __restrict__ counters) {
   using C = Cfg<WM>;
   constexpr int BM = C::BM, P = C::kParts, S = C::kAStages, D = C::kAhead;
   // Activation stages: one LDS object each, named with compile-time indices only.
@@ -359,11 +358,11 @@ hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, con
                           : nullptr;
   const dim3 grid((unsigned)(p.tiles * splits));
   if (p.wm == 4)
-    gemm_kernel<Q, G, META, 4><<<grid, Cfg<4>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
-                                                                   (int)K, y, splits, partials, counters);
+    gemm_kernel<Q, G, META, 4><<<grid, Cfg<4>::kThreads, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N,
+                                                                   (int)K, splits, y, partials, counters);
   else
-    gemm_kernel<Q, G, META, 2><<<grid, Cfg<2>::kThreads, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N,
-                                                                   (int)K, y, splits, partials, counters);
+    gemm_kernel<Q, G, META, 2><<<grid, Cfg<2>::kThreads, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N,
+                                                                   (int)K, splits, y, partials, counters);
   return hipGetLastError();
 }
 

@@ -36,9 +36,8 @@ constexpr uint32_t kOutOfRange = 0x80000000u;   // past every buffer's size: loa
 
 template <int Q, int G, int META, int MB>
 __global__ __launch_bounds__(1024) void skinny_kernel(
-    const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales, const void* __restrict__ meta, int N, int K,
-    uint16_t* __restrict__ y) {
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const void* __restrict__ meta, int M, int N, int K, uint16_t* __restrict__ y) {
   __shared__ float red[kMaxWaves][MB * 256];   // per wave: its partial D tiles, lane order
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -215,10 +214,9 @@ SplitPlan split_plan(int64_t M, int64_t N, int64_t K) {
 
 template <int Q, int G, int META, int MB>
 __global__ __launch_bounds__(64 * kSplitWaves) void skinny_split_kernel(
-    const uint16_t* __restrict__ x, int M, const uint8_t* __restrict__ codes,
-    const uint16_t* __restrict__ scales, const void* __restrict__ meta, int N, int K,
-    uint16_t* __restrict__ y, int splits, int per, float* __restrict__ partials,
-    unsigned int* __restrict__ counters) {
+    const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
+    const void* __restrict__ meta, int M, int N, int K, int splits, int per, uint16_t* __restrict__ y,
+    float* __restrict__ partials, unsigned int* __restrict__ counters) {
   constexpr int kStage = MB * 16 * 128 * 2;    // MB*16 tokens x 128 k, bf16
   __shared__ __attribute__((aligned(1024))) uint8_t xs[kChunk * kStage];
   __shared__ unsigned int arrived;
@@ -398,20 +396,20 @@ hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, c
     const int per = (int)((nsb + p.splits - 1) / p.splits);
     const dim3 grid((unsigned)p.row_blocks, (unsigned)p.splits), block(64 * kSplitWaves);
     if (p.mb == 1)
-      skinny_split_kernel<Q, G, META, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
-                                                                   y, p.splits, per, partials, counters);
+      skinny_split_kernel<Q, G, META, 1><<<grid, block, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N, (int)K,
+                                                                   p.splits, per, y, partials, counters);
     else
-      skinny_split_kernel<Q, G, META, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K,
-                                                                   y, p.splits, per, partials, counters);
+      skinny_split_kernel<Q, G, META, 2><<<grid, block, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N, (int)K,
+                                                                   p.splits, per, y, partials, counters);
     return hipGetLastError();
   }
   const int64_t nsb = (K / 32 + 3) / 4;
   const int waves = (int)std::min<int64_t>(kMaxWaves, nsb);
   const dim3 grid((unsigned)((N + 15) / 16)), block((unsigned)(64 * waves));
   if (M <= 16)
-    skinny_kernel<Q, G, META, 1><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+    skinny_kernel<Q, G, META, 1><<<grid, block, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N, (int)K, y);
   else
-    skinny_kernel<Q, G, META, 2><<<grid, block, 0, stream>>>(x, (int)M, codes, scales, zp, (int)N, (int)K, y);
+    skinny_kernel<Q, G, META, 2><<<grid, block, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N, (int)K, y);
   return hipGetLastError();
 }
 
