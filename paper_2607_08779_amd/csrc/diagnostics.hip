@@ -102,11 +102,12 @@ __global__ __launch_bounds__(kThreads, 8) void diagnostics_kernel(const In* __re
                                                                int64_t total_chunks,
                                                                int16_t* __restrict__ margin,
                                                                float* __restrict__ gain,
-                                                               unsigned long long* __restrict__ tally) {
+                                                               unsigned long long* __restrict__ tally,
+                                                               int nblocks) {
   constexpr int kLanes = G / 8;
   const bool leader = threadIdx.x % kLanes == 0;
   uint32_t packed[5] = {0, 0, 0, 0, 0};   // cell k = 3 (sign m + 1) + (sign g + 1): field k % 2 of word k / 2
-  const int64_t stride = (int64_t)gridDim.x * (kThreads * kUnroll);
+  const int64_t stride = (int64_t)nblocks * (kThreads * kUnroll);     // nblocks = gridDim.x
   // The statistics of one trip's chunks, and the tally.  total_chunks is a multiple of
   // G/8, so a group's lanes are all valid or all not.
   // Margins and gains go out through buffer stores that every lane issues: a lane other
@@ -197,7 +198,7 @@ __global__ __launch_bounds__(kThreads, 8) void diagnostics_kernel(const In* __re
                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   wait_vmcnt<0>();
   __syncthreads();
-  const unsigned int nb = gridDim.x;
+  const unsigned int nb = (unsigned int)nblocks;
   if (threadIdx.x == 0) {
     const unsigned int cls = blockIdx.x % kClasses;
     const unsigned int members = (nb - cls + kClasses - 1) / kClasses;   // blocks of this class
@@ -259,7 +260,7 @@ hipError_t diagnose(const In* W, int64_t total_chunks, int16_t* margin, float* g
   const int64_t blocks = std::min<int64_t>(needed, kMaxBlocks);
   if ((needed + blocks - 1) / blocks > kMaxTrips) return hipErrorInvalidValue;   // past about 2^38 weights
   diagnostics_kernel<In, Q, G><<<dim3((unsigned)blocks), kThreads, 0, nullptr>>>(W, total_chunks, margin,
-                                                                                gain, tally);
+                                                                                gain, tally, (int)blocks);
   return hipGetLastError();
 }
 
