@@ -212,8 +212,9 @@ def diagnostics_bytes(N, K, g):
 def stream_ceiling(torch, dev, nbytes: int, copies: int, reps: int):
     """The practical HBM ceiling next to the GEMV: a plain streaming read (the
     measurement-only ssq_bench_stream_read kernel) of `copies` distinct buffers of the
-    GEMV's byte count, replayed in a HIP graph like the GEMV phase.  None if the
-    measurement library is not built."""
+    GEMV's byte count, each launch also storing about as many bytes as the GEMV's
+    output, replayed in a HIP graph like the GEMV phase.  None if the measurement
+    library is not built."""
     import ctypes
     path = os.path.join(ROOT, "paper_2607_08779_amd", "libssq_bench.so")
     if not os.path.exists(path):
@@ -221,8 +222,10 @@ def stream_ceiling(torch, dev, nbytes: int, copies: int, reps: int):
     lib = ctypes.CDLL(path)
     lib.ssq_bench_stream_read.restype = ctypes.c_int
     lib.ssq_bench_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    lib.ssq_bench_stream_read_sink_words.restype = ctypes.c_int64
+    lib.ssq_bench_stream_read_sink_words.argtypes = [ctypes.c_int64]
     bufs = [torch.full((nbytes // 4,), i + 1, dtype=torch.int32, device=dev) for i in range(copies)]
-    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    sink = torch.zeros(max(1, lib.ssq_bench_stream_read_sink_words(nbytes)), dtype=torch.int32, device=dev)
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
         def run():

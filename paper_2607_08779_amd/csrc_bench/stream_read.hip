@@ -2,8 +2,10 @@
 // read of a device buffer, the practical HBM ceiling that bench.py reports next to
 // the decode GEMV (same bytes per launch, same number of distinct buffers, same graph
 // replay).  Each thread reads four 16-byte items 256 items apart (non-temporal, like
-// the GEMV's code loads); the XOR of everything read stays live through a store that
-// only a data word equal to a fixed constant would trigger.
+// the GEMV's code loads); each block stores the XOR of what it read as one dword, so
+// a launch also writes about as many bytes as the GEMV's output (4 bytes per 16 KB
+// read: 8 KB for 33 MB, against the GEMV's 2 bytes per row), and like the GEMV it pays
+// for those stores to land before the next launch starts.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -26,17 +28,22 @@ __global__ __launch_bounds__(kThreads) void stream_read_kernel(const u32x4* __re
       acc ^= v.x ^ v.y ^ v.z ^ v.w;
     }
   }
-  if (acc == 0x9E3779B9u) sink[0] = acc;
+  if (threadIdx.x == 0) sink[blockIdx.x] = acc;
 }
 
 }  // namespace
 
 // Reads bytes/16 16-byte items of p (device, 16-byte aligned) on `stream`; sink is a
-// device word that the kernel may write.  Returns 0 or a hipError_t value.
+// device array of at least ssq_bench_stream_read_sink_words(bytes) dwords that the
+// kernel writes.  Returns 0 or a hipError_t value.
+extern "C" int64_t ssq_bench_stream_read_sink_words(int64_t bytes) {
+  return (bytes / 16 + kThreads * kItems - 1) / (kThreads * kItems);
+}
+
 extern "C" int ssq_bench_stream_read(const void* p, int64_t bytes, uint32_t* sink, hipStream_t stream) {
   const int64_t n16 = bytes / 16;
   if (n16 <= 0) return 0;
-  const int64_t blocks = (n16 + kThreads * kItems - 1) / (kThreads * kItems);
+  const int64_t blocks = ssq_bench_stream_read_sink_words(bytes);
   stream_read_kernel<<<dim3((unsigned)blocks), kThreads, 0, stream>>>(static_cast<const u32x4*>(p), n16, sink);
   return (int)hipGetLastError();
 }
