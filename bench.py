@@ -196,10 +196,14 @@ def meta_bytes_per_group(mode_name):
 
 
 def matmul_bytes(M, N, K, q, g, meta):
+    """Algorithmic bytes of one M x N x K matmul on packed weights: codes, fp16 scales and
+    `meta` bytes per group, bf16 activations read and bf16 outputs written."""
     return N * K * q // 8 + (2 + meta) * N * K // g + 2 * M * K + 2 * M * N
 
 
 def quantize_bytes(N, K, q, g, meta):
+    """Algorithmic bytes of quantizing bf16 W[N, K]: weights read, codes, scales and
+    `meta` bytes per group written."""
     return 2 * N * K + N * K * q // 8 + (2 + meta) * N * K // g
 
 
@@ -557,11 +561,11 @@ def main() -> int:
     t_m = sum(e[3].elapsed_time(e[4]) for e in events) / 1e3
     t_step = sum(e[0].elapsed_time(e[4]) for e in events) / 1e3 / args.steps
 
-    zp_bytes = meta_bytes_per_group(args.mode) * N * K // g
-    gemv_bytes = N * K * q // 8 + 2 * N * K // g + zp_bytes + 2 * K + 2 * N
-    quant_bytes = 2 * N * K + N * K * q // 8 + 2 * N * K // g + zp_bytes
+    meta = meta_bytes_per_group(args.mode)
+    gemv_bytes = matmul_bytes(1, N, K, q, g, meta)
+    quant_bytes = quantize_bytes(N, K, q, g, meta)
     gemm_flops = 2 * args.gemm_m * N * K
-    batched_bytes = N * K * q // 8 + 2 * N * K // g + zp_bytes + 2 * args.batched_m * (K + N)
+    batched_bytes = matmul_bytes(args.batched_m, N, K, q, g, meta)
     n_gemv = args.steps * args.layers
     n_gemm = args.steps * args.gemm_layers
 
