@@ -32,6 +32,8 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}",
 ]
+# Per-source additions to FLAGS.
+FILE_FLAGS: dict[str, list[str]] = {}
 
 
 def hipcc() -> str:
@@ -45,35 +47,33 @@ def sources() -> list[str]:
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
-def _compile(src: str, build_dir: str, extra_flags: list[str]) -> str:
+def _compile(src: str, build_dir: str) -> str:
     obj = os.path.join(build_dir, os.path.basename(src) + ".o")
-    cmd = [hipcc(), *FLAGS, *extra_flags, "-c", src, "-o", obj]
+    cmd = [hipcc(), *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")
     return obj
 
 
-def build(verbose: bool = False, lib_path: str = LIB, build_dir: str = BUILD,
-          extra_flags: list[str] | None = None) -> str:
+def build(verbose: bool = False, lib_path: str = LIB, build_dir: str = BUILD) -> str:
     """Compile every HIP source and link libssq.so (or lib_path); returns the library path.
-    extra_flags (e.g. -D tuning macros) go to every compile.  The default build also
-    links bench.py's measurement library (libssq_bench.so)."""
-    path = _link(sources(), lib_path, build_dir, extra_flags)
+    The default build also links bench.py's measurement library (libssq_bench.so)."""
+    path = _link(sources(), lib_path, build_dir)
     if verbose:
         print(f"built {path}")
     if lib_path == LIB:
         bench_srcs = sorted(os.path.join(BENCH_SRC, f) for f in os.listdir(BENCH_SRC) if f.endswith(".hip"))
-        bpath = _link(bench_srcs, BENCH_LIB, os.path.join(build_dir, "bench"), [])
+        bpath = _link(bench_srcs, BENCH_LIB, os.path.join(build_dir, "bench"))
         if verbose:
             print(f"built {bpath}")
     return path
 
 
-def _link(srcs: list[str], lib_path: str, build_dir: str, extra_flags: list[str] | None) -> str:
+def _link(srcs: list[str], lib_path: str, build_dir: str) -> str:
     os.makedirs(build_dir, exist_ok=True)
     with ThreadPoolExecutor(min(8, len(srcs))) as ex:
-        objs = list(ex.map(lambda f: _compile(f, build_dir, extra_flags or []), srcs))
+        objs = list(ex.map(lambda f: _compile(f, build_dir), srcs))
     tmp = lib_path + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -179,10 +179,7 @@ __device__ __forceinline__ void block_pairs(const Block<Q>& b, uint32_t magic, u
 // points) and one the activations; loads past a descriptor's range return zeros.
 // Lanes past the end of a row point their loads out of range, so rows and blocks
 // beyond the matrix contribute exact zeros.
-#ifndef SSQ_GEMV_ROWS
-#define SSQ_GEMV_ROWS 4          // rows per workgroup
-#endif
-constexpr int kRows = SSQ_GEMV_ROWS;
+constexpr int kRows = 4;          // rows per workgroup (the folded reduction assumes four)
 constexpr int kMaxTeam = 512;
 constexpr int kMaxWaves = kMaxTeam / 64;
 constexpr int kXChunks = 256;    // 16-byte activation chunks of one pass: 64 blocks x 64 bytes

@@ -105,6 +105,31 @@ def _check(fn: str, status: int) -> None:
         raise SSQError(fn, status)
 
 
+class _OnNullStream:
+    """Orders a null-stream entry point (ssq_quantize*, the diagnostics) with the caller's
+    current torch stream: the null stream waits for the work already queued on the
+    current stream, and the current stream waits for the launch.  PyTorch's side streams
+    are non-blocking, so without this a call inside ``torch.cuda.stream(s)`` could read
+    W before s has written it, and s could read the outputs before they are written."""
+
+    def __init__(self, device: torch.device):
+        self.other = False
+        if device.type == "cuda":        # a host tensor is refused by _ptr inside the block
+            self.cur = torch.cuda.current_stream(device)
+            self.null = torch.cuda.default_stream(device)
+            self.other = self.cur.cuda_stream != self.null.cuda_stream
+
+    def __enter__(self):
+        if self.other:
+            self.null.wait_stream(self.cur)
+        return self
+
+    def __exit__(self, *exc):
+        if self.other:
+            self.cur.wait_stream(self.null)
+        return False
+
+
 def ssq_quantize(W: torch.Tensor, group: int, q: int, mode: int,
                  out: Optional[Tuple[torch.Tensor, torch.Tensor, Optional[torch.Tensor]]] = None):
     """Quantize W [rows, cols] (bf16 or fp32, on the GPU) group-wise.
@@ -112,7 +137,8 @@ def ssq_quantize(W: torch.Tensor, group: int, q: int, mode: int,
     Returns (codes u8 [rows, cols*q/8], scales int16 [rows, cols/group] holding
     binary16 bit patterns, zp u8 [rows, cols/group] for ASYM, the binary16 minimums
     as int16 [rows, cols/group] for ASYM_MIN, else None).
-    Runs on the null stream, like the C entry point.
+    Runs on the null stream, like the C entry point, ordered after the work queued on
+    the current stream and before the work queued on it afterwards.
     """
     if W.dim() != 2 or not W.is_contiguous():
         raise ValueError("W must be a contiguous 2-D tensor")
@@ -131,11 +157,12 @@ def ssq_quantize(W: torch.Tensor, group: int, q: int, mode: int,
               if meta_dtype is not None else None)
     else:
         codes, scales, zp = out
-    if mode == ASYM_MIN:
-        fn = fn.replace("ssq_quantize", "ssq_quantize_min")
-        st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(codes), _ptr(scales), _ptr(zp))
-    else:
-        st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, mode, _ptr(codes), _ptr(scales), _ptr(zp))
+    with _OnNullStream(W.device):
+        if mode == ASYM_MIN:
+            fn = fn.replace("ssq_quantize", "ssq_quantize_min")
+            st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(codes), _ptr(scales), _ptr(zp))
+        else:
+            st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, mode, _ptr(codes), _ptr(scales), _ptr(zp))
     _check(fn, st)
     return codes, scales, zp
 
@@ -218,7 +245,8 @@ def ssq_sign_diagnostics(W: torch.Tensor, group: int, q: int, tally: bool = True
         margin = torch.empty(shape, dtype=torch.int16, device=W.device)
         gain = torch.empty(shape, dtype=torch.float32, device=W.device)
         t = torch.empty(9, dtype=torch.int64, device=W.device) if tally else None
-    st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(margin), _ptr(gain), _ptr(t))
+    with _OnNullStream(W.device):
+        st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(margin), _ptr(gain), _ptr(t))
     _check(fn, st)
     return margin, gain, (t.view(3, 3) if t is not None else None)
 
@@ -276,5 +304,7 @@ def ssq_quantize_diag(W: torch.Tensor, group: int, q: int):
     scales = torch.empty((rows, groups), dtype=torch.int16, device=W.device)
     margin = torch.empty((rows, groups), dtype=torch.int16, device=W.device)
     gain = torch.empty((rows, groups), dtype=torch.float32, device=W.device)
-    _check(fn, getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(codes), _ptr(scales), _ptr(margin), _ptr(gain)))
+    with _OnNullStream(W.device):
+        st = getattr(lib(), fn)(_ptr(W), rows, cols, group, q, _ptr(codes), _ptr(scales), _ptr(margin), _ptr(gain))
+    _check(fn, st)
     return codes, scales, margin, gain

@@ -1,4 +1,5 @@
-"""Seeded synthetic inputs: weight matrices and activations shaped like Llama3 projections.
+"""Seeded synthetic inputs: weight matrices and activations shaped like Llama3 and Qwen3
+projections.
 
 This module only draws random numbers and casts them to storage formats; it
 holds none of the quantization arithmetic, so the CPU oracle and the HIP
@@ -97,7 +98,8 @@ def activations(M: int, K: int, seed: int, bf16: bool = True) -> np.ndarray:
 
 
 # ---------------------------------------------------------------------------
-# Named workloads (shapes are the public Llama3-8B / Llama3-70B projections).
+# Named workloads (shapes are the public Llama3-8B / Llama3-70B / Qwen3-8B / Qwen3-14B
+# projections).
 # ---------------------------------------------------------------------------
 
 LLAMA3_8B = {  # name: (rows N, cols K)
@@ -109,6 +111,17 @@ LLAMA3_70B = {
     "q_proj": (8192, 8192), "k_proj": (1024, 8192), "v_proj": (1024, 8192),
     "o_proj": (8192, 8192), "gate_proj": (28672, 8192), "up_proj": (28672, 8192),
     "down_proj": (8192, 28672),
+}
+# Qwen3 dense models (Table 1 reports Qwen3 0.6B-14B): head_dim 128, 8 key/value heads.
+QWEN3_8B = {
+    "q_proj": (4096, 4096), "k_proj": (1024, 4096), "v_proj": (1024, 4096),
+    "o_proj": (4096, 4096), "gate_proj": (12288, 4096), "up_proj": (12288, 4096),
+    "down_proj": (4096, 12288),
+}
+QWEN3_14B = {
+    "q_proj": (5120, 5120), "k_proj": (1024, 5120), "v_proj": (1024, 5120),
+    "o_proj": (5120, 5120), "gate_proj": (17408, 5120), "up_proj": (17408, 5120),
+    "down_proj": (5120, 17408),
 }
 PROJ_INDEX = {name: i for i, name in enumerate(LLAMA3_8B)}
 
@@ -165,5 +178,19 @@ def llama3_70b_block() -> Workload:
                     qs=(2,), groups=(32,), ms=(1, 16), x_seed=5100)
 
 
+def qwen3_8b_block() -> Workload:
+    """All seven Qwen3-8B projections, bf16 t(5)*0.02 + 0.1% x20 outliers; q in {2,3,4},
+    g=32, M in {1, 16, 512}."""
+    return Workload("qwen3_8b_block", _llama_layers(QWEN3_8B, QWEN3_8B, 5.0, 0.02, 6000),
+                    qs=(2, 3, 4), groups=(32,), ms=(1, 16, 512), x_seed=6100)
+
+
+def qwen3_14b_block() -> Workload:
+    """All seven Qwen3-14B projections, bf16 t(5)*0.02 + 0.1% x20 outliers; q in {2,3,4},
+    g=32, M in {1, 16, 512}."""
+    return Workload("qwen3_14b_block", _llama_layers(QWEN3_14B, QWEN3_14B, 5.0, 0.02, 7000),
+                    qs=(2, 3, 4), groups=(32,), ms=(1, 16, 512), x_seed=7100)
+
+
 WORKLOADS = {w().name: w for w in (small_fp32, llama3_8b_decode, llama3_8b_block, prefill,
-                                   llama3_70b_block)}
+                                   llama3_70b_block, qwen3_8b_block, qwen3_14b_block)}

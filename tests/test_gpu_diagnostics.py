@@ -7,15 +7,35 @@ import torch
 
 from oracle import ssq_oracle as O
 from paper_2607_08779_amd import ssq, synth
-from tests.parity_common import sample_rows, to_device, widen
+from tests.parity_common import Guarded, sample_rows, to_device, widen
 
 pytestmark = pytest.mark.gpu
 
 
+def tally_of(margin: np.ndarray, gain: np.ndarray) -> np.ndarray:
+    """3x3 counts of groups by (sign of the margin, sign of the gain), -1/0/+1 -> 0/1/2."""
+    counts = np.zeros((3, 3), np.int64)
+    np.add.at(counts, (np.sign(margin).astype(np.int64).ravel() + 1,
+                       np.sign(gain).astype(np.int64).ravel() + 1), 1)
+    return counts
+
+
 def check(w_host, bf16, group, q, rows_idx=None, tag=""):
+    """Diagnostics into guarded buffers; margins and gains against the oracle (on rows_idx),
+    the tally against the oracle's (whole matrix) or against counts of the GPU's own
+    margins and gains (sampled rows).  Returns the tally."""
     W = to_device(w_host, bf16)
-    margin, gain, tally = ssq.ssq_sign_diagnostics(W, group, q)
+    rows, cols = w_host.shape
+    g_margin = Guarded((rows, cols // group), torch.int16, fill=0x5A)
+    g_gain = Guarded((rows, cols // group), torch.float32)
+    g_tally = Guarded((9,), torch.int64, fill=0x5A)
+    margin, gain, tally = ssq.ssq_sign_diagnostics(W, group, q, out=(g_margin.t, g_gain.t, g_tally.t))
     torch.cuda.synchronize()
+    for b, name in ((g_margin, "margin"), (g_gain, "gain"), (g_tally, "tally")):
+        b.check(f"{tag} {name}")
+    m_all, g_all = margin.cpu().numpy(), gain.cpu().numpy()
+    assert not np.isnan(g_all).any(), f"{tag}: gains left unwritten"
+    assert np.array_equal(tally.cpu().numpy(), tally_of(m_all, g_all)), f"{tag}: tally vs outputs"
     sel = slice(None) if rows_idx is None else rows_idx
     with np.errstate(over="ignore"):                     # a gain past binary32 rounds to inf
         ref = O.sign_diagnostics(widen(w_host[sel], bf16), group, q)
@@ -125,7 +145,7 @@ def test_diagnostics_llama3_8b_down_proj_full_size():
     w = synth.weights(spec)
     rows = sample_rows(spec.rows, 64, seed=3)
     for q in (2, 3, 4):
-        tally = check(w, True, 32, q, rows_idx=rows, tag=f"down_proj q={q}")
+        tally = check(w, True, 32, q, rows_idx=rows, tag=f"down_proj q={q}")   # tally == counts of outputs
         assert tally.sum() == spec.rows * spec.cols // 32
 
 

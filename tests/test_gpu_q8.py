@@ -9,7 +9,8 @@ import torch
 
 from oracle import ssq_oracle as O
 from paper_2607_08779_amd import ssq, synth
-from tests.parity_common import log_metric, rel_l2, sample_rows, to_device, y_to_f64
+from tests.parity_common import (Guarded, assert_within, log_metric, rel_l2, sample_rows, to_device,
+                                 y_to_f64)
 
 pytestmark = pytest.mark.gpu
 
@@ -28,8 +29,12 @@ def act_bits(M, K, seed, scale=1.0):
 
 
 def check_act(xb, tag=""):
-    qx, dx = ssq.ssq_quantize_act_q8(to_device(xb, True))
+    M, K = xb.shape
+    g_q, g_d = Guarded((M, K), torch.int8, fill=0x5A), Guarded((M, K // 32), torch.int16, fill=0x5A)
+    qx, dx = ssq.ssq_quantize_act_q8(to_device(xb, True), out=(g_q.t, g_d.t))
     torch.cuda.synchronize()
+    g_q.check(f"{tag} codes")
+    g_d.check(f"{tag} scales")
     with np.errstate(over="ignore"):
         ref = O.quantize_act_q8(O.bf16_bits_to_f32(xb))
     q, d = qx.cpu().numpy(), dx.cpu().numpy().view(np.uint16)
@@ -66,20 +71,29 @@ def check_q8_matmul(w, x_bits, group, q, mode, rows_idx=None, tag=""):
     meta = r.mins if mode == O.ASYM_MIN else r.zp
     dev_meta = None if meta is None else torch.from_numpy(
         meta.view(np.int16) if mode == O.ASYM_MIN else meta).cuda()
+    M = x_bits.shape[0]
+    g_y = Guarded((M, N), torch.bfloat16)
     y = ssq.ssq_matmul_q8(torch.from_numpy(a.q).cuda(), torch.from_numpy(a.d.view(np.int16)).cuda(),
                           torch.from_numpy(r.codes).cuda(), torch.from_numpy(r.scales.view(np.int16)).cuda(),
-                          dev_meta, N, K, group, q)
-    torch.cuda.synchronize()
+                          dev_meta, N, K, group, q, out=g_y.t)
+    g_y.check(tag)
     sel = slice(None) if rows_idx is None else rows_idx
     ref = O.matmul_q8(a.q, a.d, r.codes[sel], r.scales[sel], None if r.zp is None else r.zp[sel],
                       r.codes[sel].shape[0], K, group, q, mins=None if r.mins is None else r.mins[sel])
-    got = y_to_f64(y)[:, sel]
-    # bf16 output rounding (2^-9 relative) plus fp32 accumulation over K/32 block terms
+    assert_q8_close(y, ref, sel, tag)
+
+
+def assert_q8_close(y, ref, sel, tag):
+    """Element-wise: the integer terms are exact, so the output carries one bf16 rounding
+    (half an ulp, 2^-8 relative) plus binary32 accumulation of the K/32 block terms,
+    bounded by 1e-5 of the row's largest output."""
+    y_all = y_to_f64(y)
+    assert not np.isnan(y_all).any(), f"{tag}: output elements left unwritten"
+    got = y_all[:, sel]
     tol = 2.0 ** -8 * np.abs(ref) + 1e-5 * np.abs(ref).max(axis=1, keepdims=True) + 1e-30
-    bad = np.abs(got - ref) > tol
+    worst = assert_within(got, ref, tol, tag)
     err = rel_l2(got, ref)
-    log_metric(test="q8_matmul", tag=tag, rel_l2=err)
-    assert not bad.any(), f"{tag}: {bad.sum()} outputs off, first {np.argwhere(bad)[0]}, rel L2 {err:.2e}"
+    log_metric(test="q8_matmul", tag=tag, rel_l2=err, max_err_over_bound=worst)
     assert err <= 5e-3, f"{tag}: rel L2 {err:.2e}"
 
 
@@ -123,6 +137,4 @@ def test_q8_pipeline_llama3_8b_down_proj_full_size():
     r = O.quantize(O.bf16_bits_to_f32(wb[rows]), 32, 4, O.SIGNED_SYM)
     assert np.array_equal(codes.cpu().numpy()[rows], r.codes)
     ref = O.matmul_q8(a.q, a.d, r.codes, r.scales, None, len(rows), spec.cols, 32, 4)
-    err = rel_l2(y_to_f64(y)[:, rows], ref)
-    log_metric(test="q8_pipeline_full", rel_l2=err)
-    assert err <= 5e-3, err
+    assert_q8_close(y, ref, rows, "q8 pipeline down_proj")

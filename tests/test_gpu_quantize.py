@@ -10,7 +10,8 @@ import torch
 
 from oracle import ssq_oracle as O
 from paper_2607_08779_amd import ssq, synth
-from tests.parity_common import (assert_quant_equal, sample_rows, to_device, weights_host, widen)
+from tests.parity_common import (assert_quant_equal, guarded_quant_outputs, sample_rows, to_device,
+                                 weights_host, widen)
 
 pytestmark = pytest.mark.gpu
 
@@ -18,9 +19,15 @@ MODES = [O.SIGNED_SYM, O.UNSIGNED_SYM, O.ASYM, O.ASYM_MIN]
 
 
 def run_case(w_host, bf16, group, q, mode, rows_idx=None, tag=""):
+    """Quantize into guarded buffers (the guards must survive), compare with the oracle."""
     W = to_device(w_host, bf16)
-    out = ssq.ssq_quantize(W, group, q, mode)
+    rows, cols = w_host.shape
+    bufs = guarded_quant_outputs(rows, cols, group, q, mode)
+    out = ssq.ssq_quantize(W, group, q, mode, out=tuple(b.t if b is not None else None for b in bufs))
     torch.cuda.synchronize()
+    for b in bufs:
+        if b is not None:
+            b.check(f"{tag} q={q} g={group} mode={mode}")
     wf = widen(w_host if rows_idx is None else w_host[rows_idx], bf16)
     ref = O.quantize(wf, group, q, mode)
     assert_quant_equal(out, ref, rows_idx, tag=f"{tag} q={q} g={group} mode={mode}")
@@ -128,11 +135,29 @@ def test_llama3_8b_block_full_size(q):
 
 
 def test_llama3_70b_shapes_full_size():
-    """q=2, g=32 on the 70B q/k and down shapes (the gate/up shape shares the row length of q)."""
+    """q=2, g=32 on every distinct 70B shape: q/o 8192x8192, k/v 1024x8192, gate/up
+    28672x8192 (235 M weights) and down 8192x28672."""
     wl = synth.llama3_70b_block()
-    for name in ("q_proj", "k_proj", "down_proj"):
+    for name in ("q_proj", "k_proj", "gate_proj", "down_proj"):
         spec = wl.layers[name]
         w = synth.weights(spec)
         idx = sample_rows(spec.rows, n=16, seed=spec.seed)
         for mode in MODES:
             run_case(w, True, 32, 2, mode, rows_idx=idx, tag=name)
+
+
+def test_quantize_inside_a_side_stream():
+    """A quantize call inside torch.cuda.stream(s), between a producer and a consumer
+    queued on s, sees the producer's W and its outputs are seen by the consumer."""
+    w = random_bf16(4096, 4096, seed=21)
+    src = to_device(w, True)
+    ref_codes, ref_scales, _ = ssq.ssq_quantize(src, 32, 4, O.SIGNED_SYM)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        W = torch.empty_like(src)
+        W.copy_(src)                                    # producer on s
+        codes, scales, _ = ssq.ssq_quantize(W, 32, 4, O.SIGNED_SYM)
+        codes_seen, scales_seen = codes.clone(), scales.clone()   # consumers on s
+    s.synchronize()
+    assert torch.equal(codes_seen, ref_codes) and torch.equal(scales_seen, ref_scales)
