@@ -68,7 +68,8 @@ typedef enum {
   SSQ_OK = 0,
   SSQ_EINVAL = -1,      /* bad size, q, group, mode or zp/mode combination     */
   SSQ_EALIGN = -2,      /* a pointer violates the alignment rule above         */
-  SSQ_EHIP = -3         /* the HIP runtime reported an error at launch         */
+  SSQ_EHIP = -3,        /* the HIP runtime reported an error at launch         */
+  SSQ_ESCRATCH = -4     /* ssq_matmul_noalloc: split scratch above its maximum  */
 } ssq_status;
 
 /*
@@ -161,6 +162,26 @@ size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int
 int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                   const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * ssq_matmul_noalloc -- ssq_matmul_ws without a caller workspace, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The split reduction uses a static device array
+ * of the library instead: 64 MiB per GPU the library runs on, held until the process
+ * ends.  The call itself allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine).
+ *   x, M, codes, scales, zp, N, K, group, q, y, stream   as ssq_matmul; the current
+ *                   device must be the device of `stream`
+ * Results equal ssq_matmul_ws's with a workspace of ssq_matmul_workspace_size()
+ * bytes, bit for bit.  Returns SSQ_ESCRATCH, launching nothing, when that size
+ * exceeds 64 MiB; otherwise as ssq_matmul_ws.  Every call on one GPU shares that
+ * GPU's array and leaves its arrival counters at zero; calls that may overlap on
+ * one GPU (other streams, other threads) race and must not be issued.  The first
+ * call on a device also enqueues a small kernel on `stream` that clears the counters.
+ */
+int ssq_matmul_noalloc(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                       const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                       hipStream_t stream);
 
 /* ssq_matmul with binary32 x[M, K] and y[M, N] (fp32 accumulation and output). */
 int ssq_matmul_f32(const float* x, int64_t M, const uint8_t* codes, const uint16_t* scales,

@@ -74,13 +74,11 @@ __device__ __forceinline__ void work_item(int b, int tiles_m, int tiles_n, int s
 // Split reduction (host side).  When the output has too few tiles to give every CU
 // a workgroup, the K steps of each tile are divided among `splits` workgroups whose
 // fp32 partial tiles meet in a caller-provided workspace: [counters: one u32 per
-// tile, padded to 256 bytes][partials: tiles x splits x BM x BN fp32].
+// tile, in the fixed counter region][partials: tiles x splits x BM x BN fp32].
 // ---------------------------------------------------------------------------
 constexpr int kMinStepsPerSplit = 16;
 
 
-
-int64_t counter_bytes(int64_t tiles) { return (tiles * 4 + 255) / 256 * 256; }
 
 struct Plan {
   int wm;            // wave rows (tile height 64*wm)
@@ -99,8 +97,9 @@ Plan plan_for(int64_t M, int64_t N, int64_t K) {
   int64_t s = (p.wm == 4 ? 256 : 512) / p.tiles;
   s = std::min<int64_t>(s, steps / kMinStepsPerSplit);
   s = std::min<int64_t>(s, 8);
+  if (p.tiles > kMaxSplitCounters) s = 1;
   p.splits = (int)std::max<int64_t>(s, 1);
-  p.workspace = p.splits > 1 ? counter_bytes(p.tiles) + p.tiles * p.splits * bm * BN * 4 : 0;
+  p.workspace = p.splits > 1 ? kSplitCounterBytes + p.tiles * p.splits * bm * BN * 4 : 0;
   return p;
 }
 
@@ -354,7 +353,7 @@ hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, con
   const bool split = p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace;
   const int splits = split ? p.splits : 1;
   unsigned int* counters = static_cast<unsigned int*>(workspace);
-  float* partials = split ? reinterpret_cast<float*>(static_cast<char*>(workspace) + counter_bytes(p.tiles))
+  float* partials = split ? reinterpret_cast<float*>(static_cast<char*>(workspace) + kSplitCounterBytes)
                           : nullptr;
   const dim3 grid((unsigned)(p.tiles * splits));
   if (p.wm == 4)

@@ -186,8 +186,6 @@ constexpr int kSplitMaxSplits = 64;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-int64_t split_counter_bytes(int64_t row_blocks) { return (row_blocks * 4 + 255) / 256 * 256; }
-
 struct SplitPlan {
   int64_t row_blocks;
   int splits;
@@ -205,10 +203,9 @@ SplitPlan split_plan(int64_t M, int64_t N, int64_t K) {
   int64_t s = std::max<int64_t>(kSplitTargetWorkgroups / std::max<int64_t>(p.row_blocks, 1),
                                 (nsb + kChunk - 1) / kChunk);
   s = std::min<int64_t>(s, std::min<int64_t>(nsb, kSplitMaxSplits));
+  if (p.row_blocks > kMaxSplitCounters) s = 1;
   p.splits = (int)std::max<int64_t>(s, 1);
-  p.workspace = p.splits > 1
-                    ? split_counter_bytes(p.row_blocks) + p.row_blocks * p.splits * kSplitWaves * p.mb * 256 * 4
-                    : 0;
+  p.workspace = p.splits > 1 ? kSplitCounterBytes + p.row_blocks * p.splits * kSplitWaves * p.mb * 256 * 4 : 0;
   return p;
 }
 
@@ -391,7 +388,7 @@ hipError_t skinny_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, c
   const SplitPlan p = split_plan(M, N, K);
   if (p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace) {
     unsigned int* counters = static_cast<unsigned int*>(workspace);
-    float* partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + split_counter_bytes(p.row_blocks));
+    float* partials = reinterpret_cast<float*>(static_cast<char*>(workspace) + kSplitCounterBytes);
     const int64_t nsb = (K / 32 + 3) / 4;
     const int per = (int)((nsb + p.splits - 1) / p.splits);
     const dim3 grid((unsigned)p.row_blocks, (unsigned)p.splits), block(64 * kSplitWaves);

@@ -4,6 +4,8 @@
 // without launching anything or touching an output byte.
 #include "ssq.h"
 
+#include <mutex>
+
 #include "ssq_internal.h"
 
 namespace ssq {
@@ -83,6 +85,52 @@ int dispatch_bf16(const uint16_t* x, int64_t M, const uint8_t* codes, const uint
                                              workspace_bytes, stream));
   return status_of(ssq::launch_gemm_bf16(x, M, codes, scales, meta, N, K, group, q, y, workspace,
                                          workspace_bytes, stream));
+}
+
+// ---------------------------------------------------------------------------
+// Static split-reduction scratch of ssq_matmul_noalloc, for callers that cannot
+// allocate.  Every GPU the library runs on holds its own copy of the array until the
+// process ends; the host name `scratch` is only a handle, so its device address is
+// looked up once per device (hipGetSymbolAddress) and only that address is passed on.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::once_flag g_scratch_once[kMaxScratchDevices];
+void* g_scratch_ptr[kMaxScratchDevices];
+hipError_t g_scratch_err[kMaxScratchDevices];
+
+__global__ void zero_words(uint32_t* p, int n) {
+  const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (i < n) p[i] = 0u;
+}
+
+// Device address of the current device's scratch (null on error, with *err set).  The
+// first call on a device also clears the arrival counters at the front of the array
+// with a fill kernel on `stream` (a kernel, not a memset, so that a first call under
+// graph capture records nothing else); the split kernels return the counters to zero
+// at the end of every call, so later calls find them cleared.
+void* scratch_for_current_device(hipStream_t stream, hipError_t* err) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) {
+    *err = e != hipSuccess ? e : hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::call_once(g_scratch_once[dev], [&] {
+    void* p = nullptr;
+    hipError_t r = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (r == hipSuccess) {
+      constexpr int kWords = (int)(ssq::kSplitCounterBytes / 4);
+      zero_words<<<kWords / 256, 256, 0, stream>>>(static_cast<uint32_t*>(p), kWords);
+      r = hipGetLastError();
+    }
+    g_scratch_err[dev] = r;
+    if (r == hipSuccess) g_scratch_ptr[dev] = p;
+  });
+  *err = g_scratch_err[dev];
+  return g_scratch_ptr[dev];
 }
 
 int check_act_q8(const void* x, int64_t M, int64_t K, const void* q, const uint16_t* d) {
@@ -176,6 +224,22 @@ int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint
                        stream);
 }
 
+int ssq_matmul_noalloc(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
+                       const uint8_t* zp, int64_t N, int64_t K, int group, int q, uint16_t* y,
+                       hipStream_t stream) {
+  const int st = check_matmul(x, M, codes, scales, N, K, group, q, y);
+  if (st != SSQ_OK || M == 0 || N == 0) return st;
+  const size_t need = ssq_matmul_workspace_size(M, N, K, group, q);
+  if (need > kScratchBytes) return SSQ_ESCRATCH;
+  void* ws = nullptr;
+  if (need > 0) {
+    hipError_t e = hipSuccess;
+    ws = scratch_for_current_device(stream, &e);
+    if (ws == nullptr) return SSQ_EHIP;
+  }
+  return dispatch_bf16(x, M, codes, scales, zero_points(zp), N, K, group, q, y, ws, need, stream);
+}
+
 int ssq_matmul_min_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,
                       const uint16_t* mins, int64_t N, int64_t K, int group, int q, uint16_t* y,
                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -266,6 +330,8 @@ const char* ssq_strerror(int status) {
     case SSQ_EINVAL: return "invalid argument (size, q, group, mode, zero-point/mode mismatch or missing minimums)";
     case SSQ_EALIGN: return "misaligned pointer (W, x, y, codes need 16 bytes; scales, mins 2; workspace 256)";
     case SSQ_EHIP: return "HIP runtime error at kernel launch";
+    case SSQ_ESCRATCH: return "the split reduction needs more than ssq_matmul_noalloc's 64 MiB static scratch "
+                              "(use ssq_matmul_ws with a workspace)";
     default: return "unknown status";
   }
 }

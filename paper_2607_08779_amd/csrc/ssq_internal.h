@@ -200,6 +200,15 @@ hipError_t launch_gemm_bf16(const uint16_t* x, int64_t M, const uint8_t* codes,
 // Workspace bytes that let the GEMM split its reduction (0 when splitting would not help).
 size_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
+// Layout of a split-reduction workspace, the same for every kernel and shape: arrival
+// counters (one u32 per output tile or row block) in the first kSplitCounterBytes, fp32
+// partials after them.  Counters always sit in the same bytes, so a workspace that one
+// call left with its counters back at zero is valid for any later shape: no call's
+// partials can land where another call's counters live.  A plan that would need more
+// counters than fit does not split.
+constexpr int64_t kSplitCounterBytes = 65536;
+constexpr int64_t kMaxSplitCounters = kSplitCounterBytes / 4;
+
 
 // Token counts 2..kSkinnyMaxM run the skinny-M kernels (weights dequantized once into
 // MFMA operands; with a workspace the reduction is split across workgroups).

@@ -41,6 +41,7 @@ _EXPORTS = {
                                      ctypes.c_size_t, ctypes.c_void_p]),
     "ssq_strerror": (ctypes.c_char_p, [ctypes.c_int]),
 }
+_EXPORTS["ssq_matmul_noalloc"] = _EXPORTS["ssq_matmul"]
 _Q_MIN = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_int,
                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p])
 _EXPORTS["ssq_quantize_min"] = _Q_MIN
@@ -213,6 +214,24 @@ def ssq_matmul(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
         st = getattr(lib(), fn)(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
                                 _ptr(y), _stream(x.device))
     _check(fn, st)
+    return y
+
+
+def ssq_matmul_noalloc(x: torch.Tensor, codes: torch.Tensor, scales: torch.Tensor,
+                       zp: Optional[torch.Tensor], N: int, K: int, group: int, q: int,
+                       out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """ssq_matmul for bf16 x whose split reduction uses the library's static scratch
+    (``ssq_matmul_noalloc``) instead of a workspace; symmetric or u8 zero-point weights.
+    With ``out`` given, the call allocates nothing."""
+    if x.dim() != 2 or not x.is_contiguous() or x.shape[1] != K or x.dtype != torch.bfloat16:
+        raise ValueError("x must be a contiguous bfloat16 [M, K] tensor")
+    if zp is not None and zp.dtype != torch.uint8:
+        raise TypeError("zp must be uint8 zero points or None")
+    M = x.shape[0]
+    y = torch.empty((M, N), dtype=x.dtype, device=x.device) if out is None else out
+    st = lib().ssq_matmul_noalloc(_ptr(x), M, _ptr(codes), _ptr(scales), _ptr(zp), N, K, group, q,
+                                  _ptr(y), _stream(x.device))
+    _check("ssq_matmul_noalloc", st)
     return y
 
 

@@ -11,7 +11,8 @@ from paper_2607_08779_amd import ssq
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "ssq.h")
 
-EINVAL, EALIGN = -1, -2
+EINVAL, EALIGN, ESCRATCH = -1, -2, -4
+COUNTERS = 65536                    # fixed arrival-counter region at the front of a workspace
 P16 = ctypes.c_void_p(1 << 20)      # aligned dummy pointers: never dereferenced, because
 P2 = ctypes.c_void_p((1 << 20) + 2)  # every call below fails validation first
 
@@ -25,7 +26,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_matmul_min",
                                     "ssq_matmul_min_f32", "ssq_matmul_min_ws",
-                                    "ssq_matmul_q8", "ssq_matmul_q8_min",
+                                    "ssq_matmul_noalloc", "ssq_matmul_q8", "ssq_matmul_q8_min",
                                     "ssq_matmul_workspace_size", "ssq_matmul_ws",
                                     "ssq_quantize", "ssq_quantize_act_q8",
                                     "ssq_quantize_diag", "ssq_quantize_diag_f32",
@@ -41,7 +42,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_strerror_never_null():
-    for st in (0, -1, -2, -3, 7, -99):
+    for st in (0, -1, -2, -3, -4, 7, -99):
         assert isinstance(ssq.ssq_strerror(st), str) and ssq.ssq_strerror(st)
 
 
@@ -102,14 +103,29 @@ def test_workspace_size_rules():
     lib = ssq.lib()
     # M=512 x N=4096 has 64 output tiles of 256x128, too few for 256 CUs: split 4 ways
     n = lib.ssq_matmul_workspace_size(512, 4096, 14336, 32, 4)
-    assert n == 256 + 64 * 4 * 256 * 128 * 4           # counters (64 x u32, padded) + partials
+    assert n == COUNTERS + 64 * 4 * 256 * 128 * 4      # fixed counter region + partials
     assert lib.ssq_matmul_workspace_size(2048, 14336, 4096, 32, 4) == 0   # enough tiles
     assert lib.ssq_matmul_workspace_size(1, 4096, 14336, 32, 4) == 0      # GEMV never splits
     # batched decode: 32 row blocks of 128 rows, 16 slices of K, one 16-token block
-    assert lib.ssq_matmul_workspace_size(16, 4096, 14336, 32, 4) == 256 + 32 * 16 * 8 * 256 * 4
-    assert lib.ssq_matmul_workspace_size(32, 4096, 14336, 32, 4) == 256 + 32 * 16 * 8 * 512 * 4
+    assert lib.ssq_matmul_workspace_size(16, 4096, 14336, 32, 4) == COUNTERS + 32 * 16 * 8 * 256 * 4
+    assert lib.ssq_matmul_workspace_size(32, 4096, 14336, 32, 4) == COUNTERS + 32 * 16 * 8 * 512 * 4
     assert lib.ssq_matmul_workspace_size(512, 4096, 48, 32, 4) == 0       # invalid K
     assert lib.ssq_matmul_workspace_size(512, 4096, 256, 32, 4) == 0      # too few steps
+
+
+def test_noalloc_rejects_problems_beyond_its_scratch():
+    """ssq_matmul_noalloc refuses, before any HIP call, a split that needs more than its
+    64 MiB static scratch: 131072 x 8192 at M = 16 needs 1024 row blocks x 8 slices of
+    partials (exactly 64 MiB) plus the counter region."""
+    lib = ssq.lib()
+    need = lib.ssq_matmul_workspace_size(16, 131072, 8192, 32, 4)
+    assert need == COUNTERS + (64 << 20)
+    st = lib.ssq_matmul_noalloc(P16, 16, P16, P16, None, 131072, 8192, 32, 4, P16, None)
+    assert st == ESCRATCH and "64 MiB" in ssq.ssq_strerror(st)
+    # invalid arguments are still reported as such
+    assert lib.ssq_matmul_noalloc(P16, 16, P16, P16, None, 8, 48, 32, 4, P16, None) == EINVAL
+    assert lib.ssq_matmul_noalloc(P2, 16, P16, P16, None, 8, 64, 32, 4, P16, None) == EALIGN
+    assert lib.ssq_matmul_noalloc(None, 0, None, None, None, 8, 64, 32, 4, None, None) == 0
 
 
 def test_matmul_ws_rejects_misaligned_workspace():
