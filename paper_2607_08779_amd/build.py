@@ -25,14 +25,15 @@ ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",
     "-ffp-contract=off",                      # every fma in the kernels is written out
-    "-mllvm", "-amdgpu-mfma-vgpr-form=1",     # MFMA accumulators in VGPRs: no AGPR copies in loops
     # the first kernel arguments arrive in SGPRs at dispatch (no scalar load before the
     # first address is known; ~0.2 us per decode GEMV launch)
     "-mllvm", "-amdgpu-kernarg-preload-count=16",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}",
 ]
-# Per-source additions to FLAGS.
+# MFMA accumulators in VGPRs (no AGPR copies in loops); a kernel that needs AGPR
+# accumulators would take an entry in FILE_FLAGS without it.
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 FILE_FLAGS: dict[str, list[str]] = {}
 
 
@@ -49,7 +50,7 @@ def sources() -> list[str]:
 
 def _compile(src: str, build_dir: str) -> str:
     obj = os.path.join(build_dir, os.path.basename(src) + ".o")
-    cmd = [hipcc(), *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
+    cmd = [hipcc(), *FLAGS, *FILE_FLAGS.get(os.path.basename(src), VGPR_FORM), "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")
@@ -79,6 +80,14 @@ def _link(srcs: list[str], lib_path: str, build_dir: str) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    # A kernel whose host launch stub the compiler did not emit links fine but fails at
+    # load time; refuse such a library here.
+    nm = shutil.which("nm") or "/opt/rocm/llvm/bin/llvm-nm"
+    r = subprocess.run([nm, "-D", "--undefined-only", tmp], capture_output=True, text=True)
+    stubs = [l for l in r.stdout.splitlines() if "__device_stub__" in l]
+    if stubs:
+        os.remove(tmp)
+        raise RuntimeError(f"{lib_path}: kernel launch stubs missing from the host objects:\n" + "\n".join(stubs[:5]))
     os.replace(tmp, lib_path)
     return lib_path
 

@@ -152,6 +152,33 @@ def test_gemv_unaligned_metadata(mode):
     assert torch.equal(y, y_ref)
 
 
+@pytest.mark.parametrize("M", [16, 96, 300])
+@pytest.mark.parametrize("mode", MODES)
+def test_matmul_unaligned_metadata(M, mode):
+    """Batched decode and the GEMM with scales (and zero points or minimums) that start
+    off a 4-byte boundary (offsets of one element): the result equals the aligned call
+    bit for bit, with and without the split workspace."""
+    N, K = 200, 1056
+    w = rand_w(N, K, seed=31)
+    codes, scales, zp = ssq.ssq_quantize(to_device(w, True), 32, 4, mode)
+    X = to_device(synth.activations(M, K, seed=32), True)
+    s_buf = torch.zeros(scales.numel() + 8, dtype=scales.dtype, device="cuda")
+    s_off = s_buf[1:1 + scales.numel()].view(scales.shape)
+    s_off.copy_(scales)
+    z_off = None
+    if zp is not None:
+        z_buf = torch.zeros(zp.numel() + 16, dtype=zp.dtype, device="cuda")
+        z_off = z_buf[3:3 + zp.numel()].view(zp.shape) if zp.dtype == torch.uint8 else \
+            z_buf[1:1 + zp.numel()].view(zp.shape)
+        z_off.copy_(zp)
+    assert s_off.data_ptr() % 4 != 0
+    for ws in (None, ssq.ssq_matmul_workspace(M, N, K, 32, 4)):
+        y_ref = ssq.ssq_matmul(X, codes, scales, zp, N, K, 32, 4, workspace=ws)
+        y = ssq.ssq_matmul(X, codes, s_off, z_off, N, K, 32, 4, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), y_ref.view(torch.int16))
+
+
 @pytest.mark.parametrize("q", [2, 3, 4])
 @pytest.mark.parametrize("group", [32, 128])
 @pytest.mark.parametrize("mode", MODES)
