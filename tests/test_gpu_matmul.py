@@ -63,10 +63,11 @@ def compare_matmul(y, x_real, ref_q, sel, K, group, q, bf16_x, tag):
 
 
 def check_matmul(w_host, x_host, group, q, mode, rows_idx=None, bf16_w=True, bf16_x=True, tag="",
-                 workspace=False, repeat=1):
+                 workspace=False, repeat=1, need_split=True):
     """Quantize on the GPU, multiply on the GPU, compare with the oracle on rows_idx.
     With workspace=True the split-reduction entry point runs `repeat` times on one
-    workspace and every result is checked."""
+    workspace and every result is checked (need_split=False: shapes whose plan does not
+    split run without one)."""
     N, K = w_host.shape
     M = x_host.shape[0]
     W = to_device(w_host, bf16_w)
@@ -75,8 +76,8 @@ def check_matmul(w_host, x_host, group, q, mode, rows_idx=None, bf16_w=True, bf1
     ws = None
     if workspace:
         nbytes = ssq.ssq_matmul_workspace_size(M, N, K, group, q)
-        assert nbytes > 0, "shape chosen to need a split"
-        ws = Guarded((nbytes,), torch.uint8, fill=0)
+        assert nbytes > 0 or not need_split, "shape chosen to need a split"
+        ws = Guarded((nbytes,), torch.uint8, fill=0) if nbytes else None
     sel = np.arange(N) if rows_idx is None else rows_idx
     ref_q = O.quantize(widen(w_host[sel], bf16_w), group, q, mode)
     assert_quant_equal((codes, scales, zp), ref_q, None if rows_idx is None else sel, tag=tag)
@@ -421,7 +422,7 @@ def test_llama3_70b_matmul_full_size(M, workspace):
         w = synth.weights(spec)
         x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
         check_matmul(w, x, 32, 2, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=24, seed=M),
-                     tag=f"70b {name} M={M}", workspace=workspace, repeat=2 if workspace else 1)
+                     tag=f"70b {name} M={M}", workspace=workspace, repeat=2 if workspace else 1, need_split=False)
 
 
 @pytest.mark.parametrize("q", [2, 3, 4])

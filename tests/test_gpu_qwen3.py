@@ -55,7 +55,7 @@ def test_qwen3_batched_decode_full_size(model):
         x = synth.activations(16, spec.cols, seed=wl.x_seed + 16)
         for ws in (False, True):
             check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=24, seed=16),
-                         tag=f"{model} {name} M=16 ws={ws}", workspace=ws)
+                         tag=f"{model} {name} M=16 ws={ws}", workspace=ws, need_split=False)
 
 
 @pytest.mark.parametrize("model", list(WORKLOADS))
