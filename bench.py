@@ -9,8 +9,11 @@ signed symmetric scales):
   2. decode: one GEMV (M=1) through each of ``--layers`` distinct quantized
      copies of that matrix, like one token through a stack of layers
                                                          -> ssq_matmul, M=1
-  3. prefill: a GEMM with M=512 tokens through ``--gemm-layers`` of the copies
+  3. batched decode: M=16 tokens through each of the copies -> ssq_matmul, M=16
+  4. prefill: a GEMM with M=512 tokens through ``--gemm-layers`` of the copies
                                                          -> ssq_matmul, M=512
+  5. the decode GEMV on the Llama3-70B down-projection (8192x28672), through
+     ``--layers70b`` quantized copies                    -> ssq_matmul, M=1
 
 The layer copies total more than the 256 MB Infinity Cache, so the GEMV
 streams its codes from HBM.  The GEMV and GEMM launches of a step are captured
@@ -18,14 +21,16 @@ once in a HIP graph and replayed (Python cannot issue microsecond kernels fast
 enough to keep the GPU busy).  Each phase is bracketed by HIP events on the
 stream its kernels run on; a kernel's average duration is the phase time over
 its launches.  ``value`` is the decode GEMV's algorithmic HBM bandwidth (codes
-+ scales + x + y bytes per launch over its average duration); the GEMM's
-TFLOP/s and the quantize kernel's bandwidth are reported beside it.
++ scales + x + y bytes per launch over its average duration); the other phases
+are reported beside it, each with its roofline.  The CPU oracle is timed first,
+on one thread and on every host thread (up to 16), before the GPU is touched.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
        python bench.py --sweep      (format sweep: all Llama3-8B projections at every
                                      q, g and mode; the sign-rule diagnostics of that
                                      block; the prefill GEMM per mode; the Llama3-70B
-                                     block at q=2 -- one JSON line; --sweep-parts picks)
+                                     block at q=2; the Qwen3-8B and -14B blocks; a GEMV
+                                     K-sweep -- one JSON line; --sweep-parts picks)
 """
 from __future__ import annotations
 
@@ -81,6 +86,38 @@ def measured_traffic(kind: str, mode: str = "signed_sym"):
     return entry.get("hbm_bytes_per_launch")
 
 
+TRACE_FILE = os.path.join(ROOT, "profiles", "kernel_trace.json")
+
+
+def traced_launch_us(kind: str, mode: str = "signed_sym"):
+    """A kernel's average duration from the committed rocprofv3 kernel trace of this
+    benchmark, or None if absent or taken on a different version of its source.  The
+    trace times the kernel alone; the HIP events of the phases also hold the gaps
+    between the graph's kernel nodes."""
+    if mode != "signed_sym":
+        return None
+    try:
+        with open(TRACE_FILE) as f:
+            entry = json.load(f).get(kind)
+    except (OSError, ValueError):
+        return None
+    if not entry or entry.get("source_sha") != kernel_source_sha(KERNEL_SOURCES[kind.split(":")[0]]):
+        return None
+    return entry.get("avg_us")
+
+
+def add_trace_frac(roof: dict, kind: str, mode: str, work: float) -> None:
+    """Put the trace-timed rate and fraction of peak beside the event-timed ones."""
+    us = traced_launch_us(kind, mode)
+    roof["trace_avg_launch_us"] = us
+    if us is None:
+        roof["trace_frac"] = None
+        return
+    rate = work / (us * 1e-6) / (1e9 if roof["unit"] == "GB/s" else 1e12)
+    roof["trace_achieved"] = round(rate, 2)
+    roof["trace_frac"] = round(rate / roof["peak"], 4)
+
+
 def parse_args():
     p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     p.add_argument("--gpus", type=int, default=1)
@@ -94,42 +131,87 @@ def parse_args():
     p.add_argument("--batched-m", type=int, default=16, help="tokens of the batched-decode phase")
     p.add_argument("--sweep", action="store_true",
                    help="format sweep over the Llama3 shapes instead of the headline step")
-    p.add_argument("--sweep-parts", default="formats,diagnostics,q8,prefill,70b",
+    p.add_argument("--sweep-parts", default="formats,diagnostics,q8,prefill,70b,qwen3,ksweep",
                    help="comma list of sweep parts: formats (8B block, every format), diagnostics "
                         "(sign-rule statistics of the 8B block), q8 (Q8_0 activations, integer "
-                        "GEMV against the bf16 GEMV), prefill, 70b")
-    p.add_argument("--phases", default="quantize,gemv,batched,gemm",
+                        "GEMV against the bf16 GEMV), prefill, 70b, qwen3 (Qwen3-8B and -14B "
+                        "blocks), ksweep (W4 GEMV at N=4096 over K next to a streaming read)")
+    p.add_argument("--phases", default="quantize,gemv,batched,gemm,gemv70b",
                    help="comma list of phases to run (profiling runs isolate one kernel); "
-                        "'copy' adds a plain 256 MiB device copy used to calibrate byte counters")
+                        "gemv70b is the decode GEMV on the Llama3-70B down-projection "
+                        "(8192x28672); 'copy' adds a plain 256 MiB device copy used to "
+                        "calibrate byte counters")
+    p.add_argument("--layers70b", type=int, default=4,
+                   help="distinct quantized copies of the 8192x28672 matrix (gemv70b phase)")
     return p.parse_args()
 
 
-def cpu_baseline(w_bits: np.ndarray, x_bits: np.ndarray, N: int, K: int, g: int, q: int,
-                 mode: int, gemv_bytes_per_row: float, budget_s: float = 12.0) -> dict:
-    """Time the CPU oracle (single thread) on a bounded sample of the same workload:
-    quantize + binary64 GEMV over the first 2048 rows, repeated until ~budget_s."""
+def _oracle_rows(args):
+    """Quantize rows [lo, hi) of the bf16 matrix with the oracle and run its binary64 GEMV
+    on them, `reps` times; returns (quantize seconds, GEMV seconds).  One thread."""
+    w_bits, x_bits, lo, hi, K, g, q, mode, reps = args
     from threadpoolctl import threadpool_limits
 
     from oracle import ssq_oracle as O
 
-    rows = min(N, 2048)
-    wf_sample = w_bits[:rows]
     xf = O.bf16_bits_to_f32(x_bits)
     t_quant = t_gemv = 0.0
-    reps = 0
     with threadpool_limits(limits=1):
-        t_start = time.perf_counter()
-        while reps < 1 or (time.perf_counter() - t_start < budget_s and reps < 8):
+        for _ in range(reps):
             t0 = time.perf_counter()
-            r = O.quantize(O.bf16_bits_to_f32(wf_sample), g, q, mode)
+            r = O.quantize(O.bf16_bits_to_f32(w_bits[lo:hi]), g, q, mode)
             t1 = time.perf_counter()
-            O.matmul(xf, r.codes, r.scales, r.zp, rows, K, g, q, mins=r.mins)
-            t2 = time.perf_counter()
+            O.matmul(xf, r.codes, r.scales, r.zp, hi - lo, K, g, q, mins=r.mins)
             t_quant += t1 - t0
-            t_gemv += t2 - t1
-            reps += 1
-    gemv_bytes = gemv_bytes_per_row * rows
-    quant_bytes = rows * K * (2 + q / 8 + 2 / g + ({2: 1, 3: 2}.get(mode, 0) / g))
+            t_gemv += time.perf_counter() - t1
+    return t_quant, t_gemv
+
+
+def host_worker_count() -> int:
+    """Host threads this process may run on, at most 16 (one GPU's share of the host)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(w_bits: np.ndarray, x_bits: np.ndarray, N: int, K: int, g: int, q: int,
+                 mode: int, gemv_bytes_per_row: float, budget_s: float = 10.0) -> dict:
+    """Time the CPU oracle on a bounded sample of the same workload, quantize + binary64
+    GEMV, in two legs of about budget_s each: one thread on rows 0..2047, and every host
+    thread (up to 16 processes, one thread each) on all rows, split into equal row slices.
+    Must run before the process touches the GPU: the all-cores leg forks."""
+    import multiprocessing as mp
+
+    quant_bytes_per_row = K * (2 + q / 8 + 2 / g + ({2: 1, 3: 2}.get(mode, 0) / g))
+    rows1 = min(N, 2048)
+    t_q1, t_v1 = _oracle_rows((w_bits, x_bits, 0, rows1, K, g, q, mode, 1))
+    reps1 = max(1, min(8, int(budget_s / max(t_q1 + t_v1, 1e-3))))
+    if reps1 > 1:
+        t_q1, t_v1 = _oracle_rows((w_bits, x_bits, 0, rows1, K, g, q, mode, reps1))
+    else:
+        reps1 = 1
+    single = {
+        "value": round(gemv_bytes_per_row * rows1 * reps1 / t_v1 / 1e9, 6), "unit": "GB/s", "cores": 1,
+        "kind": "oracle",
+        "sample": (f"oracle quantize + binary64 GEMV on rows 0..{rows1 - 1} of the {N}x{K} matrix "
+                   f"({rows1}/{N} of the workload), {reps1} repetition(s), one thread"),
+        "quantize_gbs": round(quant_bytes_per_row * rows1 * reps1 / t_q1 / 1e9, 6),
+        "seconds": round(t_q1 + t_v1, 2)}
+
+    P = host_worker_count()
+    bounds = np.linspace(0, N, P + 1).astype(int)
+    per_pass = (t_q1 + t_v1) / reps1 * N / rows1 / P         # estimated seconds per slice pass
+    repsP = max(1, min(8, int(budget_s / max(per_pass, 1e-3))))
+    jobs = [(w_bits, x_bits, int(bounds[i]), int(bounds[i + 1]), K, g, q, mode, repsP) for i in range(P)]
+    t0 = time.perf_counter()
+    with mp.get_context("fork").Pool(P) as pool:
+        parts = pool.map(_oracle_rows, jobs)
+    wall = time.perf_counter() - t0
+    # each slice's quantize and GEMV times; the slowest slice bounds the parallel pass
+    t_qP = max(p[0] for p in parts)
+    t_vP = max(p[1] for p in parts)
     cpu_model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -140,14 +222,16 @@ def cpu_baseline(w_bits: np.ndarray, x_bits: np.ndarray, N: int, K: int, g: int,
     except OSError:
         pass
     return {
-        "value": round(gemv_bytes * reps / t_gemv / 1e9, 6),
+        "value": round(gemv_bytes_per_row * N * repsP / t_vP / 1e9, 6),
         "unit": "GB/s",
-        "cores": 1,
+        "cores": P,
         "kind": "oracle",
-        "sample": (f"oracle quantize + binary64 GEMV on rows 0..{rows - 1} of the {N}x{K} matrix "
-                   f"({rows}/{N} of the workload), {reps} repetition(s), one thread"),
-        "quantize_gbs": round(quant_bytes * reps / t_quant / 1e9, 6),
-        "seconds": round(t_quant + t_gemv, 2),
+        "sample": (f"oracle quantize + binary64 GEMV on all {N} rows of the {N}x{K} matrix, "
+                   f"{P} processes of one thread on equal row slices, {repsP} repetition(s); "
+                   f"GEMV rate = GEMV bytes over the slowest slice's GEMV time"),
+        "quantize_gbs": round(quant_bytes_per_row * N * repsP / t_qP / 1e9, 6),
+        "seconds": round(wall, 2),
+        "single_thread": single,
         "host_cpu": cpu_model,
         "host_threads_available": os.cpu_count(),
     }
@@ -418,7 +502,54 @@ def sweep(args) -> int:
         del W
         torch.cuda.empty_cache()
 
-    print(json.dumps({"sweep": "format sweep on synthetic Llama3 shapes", "data": "synthetic",
+    # Qwen3-8B and Qwen3-14B blocks (the two largest Qwen3 models of Table 1): quantize,
+    # decode (M = 1, 16) and prefill (M = 512) through every projection, per layout, at
+    # q = 4 and q = 2.
+    for wl_fn in (synth.qwen3_8b_block, synth.qwen3_14b_block) if "qwen3" in parts else ():
+        wl = wl_fn()
+        names = list(wl.layers)
+        W = {n: dev_bf16(synth.weights(wl.layers[n])) for n in names}
+        for q in (4, 2):
+            for mode_name in SWEEP_MODES:
+                block_pass(wl, names, q, 32, mode_name, (1, 16, 512))
+        del W
+        torch.cuda.empty_cache()
+
+    # W4 g32 signed decode GEMV at N = 4096 over K, each K next to the streaming read of
+    # the same byte count: the marginal rate between consecutive K (bytes added over time
+    # added) shows the kernel's streaming rate with its fixed per-launch cost removed.
+    if "ksweep" in parts:
+        prev = None
+        for K in (4096, 8192, 14336, 20480, 28672):
+            spec = synth.WeightSpec(4096, K, nu=5.0, scale=0.02, outlier_frac=0.001, seed=8000 + K // 1024)
+            Wk = dev_bf16(synth.weights(spec))
+            c0 = ssq.ssq_quantize(Wk, 32, 4, ssq.SIGNED_SYM)
+            del Wk
+            b = matmul_bytes(1, 4096, K, 4, 32, 0)
+            n_copies = max(2, -(-HBM_TARGET_BYTES // b))
+            cs = [c0] + [tuple(None if t is None else t.clone() for t in c0) for _ in range(n_copies - 1)]
+            x = dev_bf16(synth.activations(1, K, seed=8100 + K // 1024))
+            y = torch.empty((1, 4096), dtype=torch.bfloat16, device=dev)
+            t = _graph_time(torch, lambda: [ssq.ssq_matmul(x, *c, 4096, K, 32, 4, out=y) for c in cs], 20) / len(cs)
+            del cs, c0
+            torch.cuda.empty_cache()
+            st = stream_ceiling(torch, dev, b // 16 * 16, n_copies, 20)
+            row = {"block": "gemv_ksweep", "op": "matmul M=1", "q": 4, "group": 32, "mode": "signed_sym",
+                   "N": 4096, "K": K, "copies": n_copies, "us": round(t * 1e6, 3), "bytes": b,
+                   "gbs": round(b / t / 1e9, 1), "frac_hbm": round(b / t / 1e9 / HBM_PEAK_GBS, 4)}
+            if st is not None:
+                row["stream_us"] = st["avg_launch_us"]
+                row["stream_gbs"] = st["gbs"]
+                row["gemv_over_stream"] = round(st["avg_launch_us"] / (t * 1e6), 4)
+            if prev is not None:
+                db = b - prev["bytes"]
+                row["marginal_gbs"] = round(db / ((row["us"] - prev["us"]) * 1e-6) / 1e9, 1)
+                if st is not None and "stream_us" in prev:
+                    row["stream_marginal_gbs"] = round(db / ((row["stream_us"] - prev["stream_us"]) * 1e-6) / 1e9, 1)
+            rows.append(row)
+            prev = row
+
+    print(json.dumps({"sweep": "format sweep on synthetic Llama3 and Qwen3 shapes", "data": "synthetic",
                       "hbm_peak_gbs": HBM_PEAK_GBS, "bf16_peak_tflops": BF16_PEAK_TFLOPS,
                       "wall_s": round(time.perf_counter() - t_start, 1), "rows": rows}), flush=True)
     return 0
@@ -436,9 +567,6 @@ def main() -> int:
 
     from paper_2607_08779_amd import ssq, synth
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    dev = torch.device("cuda:0")
     mode = ssq.MODES[args.mode]
     phases = set(args.phases.split(","))
 
@@ -447,6 +575,14 @@ def main() -> int:
     N, K, q, g = spec.rows, spec.cols, 4, 32
     w_bits = synth.weights(spec)                                   # bf16 bits, host
     x1_bits = synth.activations(1, K, seed=wl.x_seed)
+    meta = meta_bytes_per_group(args.mode)
+    gemv_bytes = matmul_bytes(1, N, K, q, g, meta)
+    # the oracle's timing forks worker processes, so it runs before anything touches the GPU
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w_bits, x1_bits, N, K, g, q, mode, gemv_bytes / N)
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
     xm_bits = synth.activations(args.gemm_m, K, seed=wl.x_seed + args.gemm_m)
     xb_bits = synth.activations(args.batched_m, K, seed=wl.x_seed + args.batched_m)
 
@@ -486,7 +622,34 @@ def main() -> int:
                 c, s, z = layers[(i * args.gemm_layers + r) % args.layers]
                 ssq.ssq_matmul(xm, c, s, z, N, K, g, q, out=ym, workspace=gemm_ws)
 
+    # Llama3-70B down-projection (8192x28672): the same GEMV on a matrix 4x larger, so
+    # the per-launch fixed cost weighs a quarter as much; copies of its quantized form
+    # stream from HBM like the 8B layers.
+    if "gemv70b" in phases:
+        wl70 = synth.llama3_70b_block()
+        s70 = wl70.layers["down_proj"]
+        N70, K70 = s70.rows, s70.cols
+        W70 = dev_bf16(synth.weights(s70))
+        first70 = ssq.ssq_quantize(W70, g, q, mode)
+        del W70
+        layers70 = [first70] + [tuple(None if t is None else t.clone() for t in first70)
+                                for _ in range(args.layers70b - 1)]
+        x70 = dev_bf16(synth.activations(1, K70, seed=wl70.x_seed + 1))
+        y70 = torch.empty((1, N70), dtype=torch.bfloat16, device=dev)
+        torch.cuda.empty_cache()
+
+    def decode_70b():
+        for c in layers70:
+            ssq.ssq_matmul(x70, *c, N70, K70, g, q, out=y70)
+
     graphs = {}
+    if "gemv70b" in phases:
+        decode_70b()
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            decode_70b()
+        graphs["gemv70b"] = gr
     for part in ("gemv", "batched", "gemm"):
         if part not in phases:
             continue
@@ -528,11 +691,15 @@ def main() -> int:
             graphs["gemm"].replay()
         if ev:
             ev[4].record()
+        if "gemv70b" in graphs:
+            graphs["gemv70b"].replay()
+        if ev:
+            ev[5].record()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -559,10 +726,9 @@ def main() -> int:
     t_v = sum(e[1].elapsed_time(e[2]) for e in events) / 1e3
     t_b = sum(e[2].elapsed_time(e[3]) for e in events) / 1e3
     t_m = sum(e[3].elapsed_time(e[4]) for e in events) / 1e3
-    t_step = sum(e[0].elapsed_time(e[4]) for e in events) / 1e3 / args.steps
+    t_70 = sum(e[4].elapsed_time(e[5]) for e in events) / 1e3
+    t_step = sum(e[0].elapsed_time(e[5]) for e in events) / 1e3 / args.steps
 
-    meta = meta_bytes_per_group(args.mode)
-    gemv_bytes = matmul_bytes(1, N, K, q, g, meta)
     quant_bytes = quantize_bytes(N, K, q, g, meta)
     gemm_flops = 2 * args.gemm_m * N * K
     batched_bytes = matmul_bytes(args.batched_m, N, K, q, g, meta)
@@ -594,6 +760,7 @@ def main() -> int:
                            "kernel": "gemv_kernel (ssq_matmul, M=1)",
                            "bytes_per_launch": gemv_bytes, "avg_launch_us": round(avg * 1e6, 3)}
         out["roofline"]["median_launch_us"], out["roofline"]["cv"] = spread(1, args.layers)
+        add_trace_frac(out["roofline"], "gemv", args.mode, gemv_bytes)
         if ceiling is not None:
             ceiling["gemv_over_stream"] = round(gbs / ceiling["gbs"], 4)
         out["ceiling_stream_read"] = ceiling
@@ -608,6 +775,7 @@ def main() -> int:
                                    "bytes_per_launch": batched_bytes, "avg_launch_us": round(avg * 1e6, 3),
                                    "tflops": round(2 * args.batched_m * N * K / avg / 1e12, 2)}
         out["roofline_batched"]["median_launch_us"], out["roofline_batched"]["cv"] = spread(2, args.layers)
+        add_trace_frac(out["roofline_batched"], "batched", args.mode, batched_bytes)
     if "gemm" in phases:
         avg = t_m / n_gemm
         tf = gemm_flops / avg / 1e12
@@ -619,6 +787,21 @@ def main() -> int:
                                 "kernel": f"gemm_kernel (ssq_matmul, M={args.gemm_m})",
                                 "flops_per_launch": gemm_flops, "avg_launch_us": round(avg * 1e6, 3)}
         out["roofline_gemm"]["median_launch_us"], out["roofline_gemm"]["cv"] = spread(3, args.gemm_layers)
+        add_trace_frac(out["roofline_gemm"], "gemm", args.mode, gemm_flops)
+    if "gemv70b" in phases:
+        avg = t_70 / (args.steps * len(layers70))
+        b70 = matmul_bytes(1, N70, K70, q, g, meta)
+        gbs = b70 / avg / 1e9
+        out["config"]["gemv70b"] = {"N": N70, "K": K70, "copies": len(layers70),
+                                    "weights": f"bf16 Student-t(5)*0.015 + 0.1% x20 outliers, seed {s70.seed}"}
+        out["roofline_gemv_70b"] = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
+                                    "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                                    "traffic": None,
+                                    "kernel": f"gemv_kernel (ssq_matmul, M=1, {N70}x{K70})",
+                                    "bytes_per_launch": b70, "avg_launch_us": round(avg * 1e6, 3)}
+        out["roofline_gemv_70b"]["median_launch_us"], out["roofline_gemv_70b"]["cv"] = \
+            spread(4, len(layers70))
+        add_trace_frac(out["roofline_gemv_70b"], "gemv:70b", args.mode, b70)
     if "quantize" in phases:
         avg = t_q / args.steps
         gbs = quant_bytes / avg / 1e9
@@ -631,8 +814,9 @@ def main() -> int:
                                     "bytes_per_launch": quant_bytes,
                                     "avg_launch_us": round(avg * 1e6, 3)}
         out["roofline_quantize"]["median_launch_us"], out["roofline_quantize"]["cv"] = spread(0, 1)
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w_bits, x1_bits, N, K, g, q, mode, gemv_bytes / N)
+        add_trace_frac(out["roofline_quantize"], "quantize", args.mode, quant_bytes)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     out["host"] = platform.node()
     print(json.dumps(out), flush=True)
     return 0

@@ -118,6 +118,44 @@ __device__ __forceinline__ float block_dot(const Block<Q>& b, const uint32_t (&x
   return acc;
 }
 
+// y + (one block's term of a row sum), from acc = sum_k x_k (base_k + u_k) (block_dot),
+// xs = sum_k x_k and xb = sum_k base_k x_k over the block, the block's scale bits and
+// its zero point or minimum bits.
+template <int Q, int META>
+__device__ __forceinline__ float add_block_term(float y, float acc, float xs, float xb, uint32_t sbits,
+                                                uint32_t zbits) {
+  const float sc = f16_bits_to_f32(sbits);
+  if constexpr (META == kMetaMin) {    // s * sum x u + m * sum x
+    y = __builtin_fmaf(sc, acc - xb, y);
+    return __builtin_fmaf(f16_bits_to_f32(zbits), xs, y);
+  } else if constexpr (Q == 2) {
+    const float o = META == kMetaZp ? (float)zbits : (float)(1 << (Q - 1));
+    return __builtin_fmaf(sc, __builtin_fmaf(-o, xs, acc - xb), y);
+  } else {
+    const float off = META == kMetaZp ? kMagicValue + (float)zbits : kMagicValue + (float)(1 << (Q - 1));
+    return __builtin_fmaf(sc, __builtin_fmaf(-off, xs, acc), y);
+  }
+}
+
+// The block sums xs and xb of one block's activations, and its pairs permuted for
+// block_dot (q = 2 pairs carry three bases, the others base 128 throughout).
+template <int Q>
+__device__ __forceinline__ void block_x(const uint32_t (&X)[16], uint32_t (&xp)[16], float& xs, float& xb) {
+  permute_x<Q>(X, xp);
+  if constexpr (Q == 2) {
+    float cs[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) cs[kClassQ2[i & 7]] = dot2(xp[i], kOnes, cs[kClassQ2[i & 7]]);
+    xs = cs[0] + cs[1] + cs[2];
+    xb = __builtin_fmaf(kBaseQ2[2], cs[2], __builtin_fmaf(kBaseQ2[1], cs[1], kBaseQ2[0] * cs[0]));
+  } else {
+    xs = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) xs = dot2(X[i], kOnes, xs);
+    xb = kMagicValue * xs;
+  }
+}
+
 // The 16 bf16 code pairs of a block in the order block_dot multiplies them (for
 // several tokens the pairs are formed once and dotted with each token's activations).
 template <int Q>
@@ -201,6 +239,25 @@ struct Stage {
 // LDS chunk holding piece p (16 bytes) of block b of a pass.
 __device__ __forceinline__ int x_slot(int b, int p) { return 4 * b + (p ^ ((b >> 2) & 3)); }
 
+// Four wavefront sums at once: swapping lane halves (32 apart, then 16 apart) folds the
+// four values of a lane into one, leaving in 16-lane row R the partials of value
+// fold4_row(16 R); four DPP steps then finish each 16-lane row, whose lane 0 (lane 16R)
+// holds the sum.
+__device__ __forceinline__ float fold4_sum(float v0, float v1, float v2, float v3) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v0), __float_as_uint(v1), false, false);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v2), __float_as_uint(v3), false, false);
+  const float s01 = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const float s23 = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+  const auto c = __builtin_amdgcn_permlane16_swap(__float_as_uint(s01), __float_as_uint(s23), false, false);
+  float v = __uint_as_float(c[0]) + __uint_as_float(c[1]);
+  v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1,0,3,2]
+  v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2,3,0,1]
+  v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
+  v = dpp_add<0x140, 0xF>(v);   // row_mirror
+  return v;
+}
+__device__ __forceinline__ int fold4_row(int lane) { return ((lane >> 4) & 1) * 2 + (lane >> 5); }
+
 // Orders LDS stores of some lanes before loads of others within one wavefront.
 __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -221,7 +278,6 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
   constexpr int kMetaSize = S::kMetaSize;
   const uint8_t* const zp = static_cast<const uint8_t*>(meta);
   constexpr int kBlocksPerGroup = S::kBlocksPerGroup;
-  constexpr float kSymOffset = kMagicValue + (float)(1 << (Q - 1));
   __shared__ float partial[kMaxWaves][kRows * T];
   extern __shared__ u32x4 stage[];
   constexpr int kWaveChunks = T * kXChunks + S::kScaleChunks + S::kZpChunks;
@@ -259,21 +315,7 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
     // block_dot (128 xs except for q = 2, whose pairs carry three bases)
     float xs[T], xb[T];
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-      permute_x<Q>(X[t], xp[t]);
-      xs[t] = 0.0f;
-      if constexpr (Q == 2) {
-        float cs[3] = {0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int i = 0; i < 16; ++i) cs[kClassQ2[i & 7]] = dot2(xp[t][i], kOnes, cs[kClassQ2[i & 7]]);
-        xs[t] = cs[0] + cs[1] + cs[2];
-        xb[t] = __builtin_fmaf(kBaseQ2[2], cs[2], __builtin_fmaf(kBaseQ2[1], cs[1], kBaseQ2[0] * cs[0]));
-      } else {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) xs[t] = dot2(X[t][i], kOnes, xs[t]);
-        xb[t] = kMagicValue * xs[t];
-      }
-    }
+    for (int t = 0; t < T; ++t) block_x<Q>(X[t], xp[t], xs[t], xb[t]);
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
       float acc[T];
@@ -289,20 +331,8 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
           for (int i = 0; i < 16; ++i) acc[t] = dot2(w[i], xp[t][i], acc[t]);
         }
       }
-      const float sc = f16_bits_to_f32(sbits[r]);
 #pragma unroll
-      for (int t = 0; t < T; ++t) {
-        if constexpr (META == kMetaMin) {    // s * sum x u + m * sum x
-          yacc[t][r] = __builtin_fmaf(sc, acc[t] - xb[t], yacc[t][r]);
-          yacc[t][r] = __builtin_fmaf(f16_bits_to_f32(zbits[r]), xs[t], yacc[t][r]);
-        } else if constexpr (Q == 2) {
-          const float o = META == kMetaZp ? (float)zbits[r] : (float)(1 << (Q - 1));
-          yacc[t][r] = __builtin_fmaf(sc, __builtin_fmaf(-o, xs[t], acc[t] - xb[t]), yacc[t][r]);
-        } else {
-          const float off = META == kMetaZp ? kMagicValue + (float)zbits[r] : kSymOffset;
-          yacc[t][r] = __builtin_fmaf(sc, __builtin_fmaf(-off, xs[t], acc[t]), yacc[t][r]);
-        }
-      }
+      for (int t = 0; t < T; ++t) yacc[t][r] = add_block_term<Q, META>(yacc[t][r], acc[t], xs[t], xb[t], sbits[r], zbits[r]);
     }
   };
 
@@ -379,23 +409,11 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
     }
     consume(X, cb, sbits, zbits);
   }
-  // Four row sums at once: swapping lane halves (32 apart, then 16 apart) folds the
-  // four values of a lane into one, leaving in 16-lane row R the partials of row
-  // (R & 1) * 2 + (R >> 1); four DPP steps then finish each 16-lane row.
   static_assert(kRows == 4, "the folded reduction handles four rows");
 #pragma unroll
   for (int t = 0; t < T; ++t) {
-    const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[t][0]), __float_as_uint(yacc[t][1]), false, false);
-    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(yacc[t][2]), __float_as_uint(yacc[t][3]), false, false);
-    const float s01 = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-    const float s23 = __uint_as_float(b[0]) + __uint_as_float(b[1]);
-    const auto c = __builtin_amdgcn_permlane16_swap(__float_as_uint(s01), __float_as_uint(s23), false, false);
-    float v = __uint_as_float(c[0]) + __uint_as_float(c[1]);
-    v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1,0,3,2]
-    v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2,3,0,1]
-    v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
-    v = dpp_add<0x140, 0xF>(v);   // row_mirror
-    if ((lane & 15) == 0) partial[wave][t * kRows + ((lane >> 4) & 1) * 2 + (lane >> 5)] = v;
+    const float v = fold4_sum(yacc[t][0], yacc[t][1], yacc[t][2], yacc[t][3]);
+    if ((lane & 15) == 0) partial[wave][t * kRows + fold4_row(lane)] = v;
   }
   __syncthreads();
   if constexpr (T == 1) {
@@ -414,6 +432,180 @@ __global__ __launch_bounds__(kMaxTeam) void gemv_kernel(const uint16_t* __restri
       y[(int64_t)t * N + row0 + r] = f32_to_bf16_bits(v);
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Activation-stationary decode GEMV (M = 1, K <= 16 x 2048), for matrices with many
+// rows per resident workgroup.
+//
+// The workgroup has C = ceil(K / 2048) wavefronts; wavefront w owns blocks 64w..64w+63
+// of every row (lane i: block 64w + i).  It loads its 4 KB of activations once (four
+// contiguous 1 KB loads, redistributed through LDS), forms their pairs and block sums
+// once, and keeps them in registers while the workgroup walks a run of PER 4-row
+// groups.  The codes, scales (and zero points or minimums) of group i+1 are in flight
+// while group i is multiplied.  After a group the wavefront folds its four rows' lane
+// partials into four sums and parks them in LDS; when the run is done the workgroup
+// adds the C wavefronts' sums of each row in wavefront order and stores y.  Per
+// 32-weight block and row a lane spends the unpack and 16 dot2 of block_dot plus the
+// scale step; the per-pass activation work of the pass-looping kernel (its LDS round
+// trip, pair permutation and block sums, and its re-read of x for every 4 rows) is
+// paid once per run of up to 32 rows.
+// ---------------------------------------------------------------------------
+
+constexpr int kStatMaxWaves = 16;      // K <= 16 x 64 blocks
+constexpr int kStatMaxGroups = 8;      // 4-row groups per workgroup
+constexpr int kCUs = 256;              // MI355X compute units
+// Two groups in registers (69 VGPRs at q = 4: seven wavefronts per SIMD), and the grid
+// sized for 28 resident wavefronts per CU.  Deeper rings (three or four groups) were
+// measured slower: the registers they take cost more wavefronts than they add loads.
+constexpr int kStatDepth = 2;
+constexpr int kStatWavesPerCU = 28;
+
+template <int Q>
+struct StatGroup {
+  Block<Q> cb[kRows];
+  uint32_t s[kRows];
+  uint32_t z[kRows];
+};
+
+// Loads of row group i of the workgroup (rows 4i..4i+3 of its run) for block j.
+template <int Q, int G, int META>
+__device__ __forceinline__ void stat_issue(StatGroup<Q>& st, int i, bool live, int j, uint32_t row_bytes,
+                                           uint32_t groups_per_row, __amdgpu_buffer_rsrc_t rc,
+                                           __amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rz) {
+  constexpr int kBlocksPerGroup = G / 32;
+  const uint32_t g = (uint32_t)(j / kBlocksPerGroup);
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    const uint32_t row = (uint32_t)(4 * i + r);
+    buffer_block_codes<Q>(rc, live ? row * row_bytes + (uint32_t)j * (4 * Q) : kOutOfRange, 0, st.cb[r].d);
+    st.s[r] = __builtin_amdgcn_raw_buffer_load_b16(rs, live ? (row * groups_per_row + g) * 2 : kOutOfRange, 0, 0);
+    if constexpr (META == kMetaMin)
+      st.z[r] = __builtin_amdgcn_raw_buffer_load_b16(rz, live ? (row * groups_per_row + g) * 2 : kOutOfRange, 0, 0);
+    else if constexpr (META == kMetaZp)
+      st.z[r] = __builtin_amdgcn_raw_buffer_load_b8(rz, live ? row * groups_per_row + g : kOutOfRange, 0, 0);
+    else
+      st.z[r] = 0u;
+  }
+}
+
+template <int Q, int META>
+__device__ __forceinline__ float stat_rows(const StatGroup<Q>& st, const uint32_t (&xp)[16], float xs, float xb,
+                                           uint32_t magic) {
+  float v[kRows];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r)
+    v[r] = add_block_term<Q, META>(0.0f, block_dot<Q>(st.cb[r], xp, magic), xs, xb, st.s[r], st.z[r]);
+  return fold4_sum(v[0], v[1], v[2], v[3]);
+}
+
+template <int Q, int G, int META, int D, int PER>
+__global__ __launch_bounds__(1024) void gemv_stat_kernel(const uint16_t* __restrict__ x,
+                                                         const uint8_t* __restrict__ codes,
+                                                         const uint16_t* __restrict__ scales,
+                                                         const void* __restrict__ meta, int N, int K,
+                                                         int groups_per_wg, uint16_t* __restrict__ y) {
+  static_assert(PER <= kStatMaxGroups && D >= 2, "run length and ring depth");
+  constexpr int kMetaSize = META == kMetaZp ? 1 : META == kMetaMin ? 2 : 0;
+  __shared__ float part[kStatMaxGroups][kStatMaxWaves][kRows];
+  const uint8_t* const zp = static_cast<const uint8_t*>(meta);
+
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int waves = (int)blockDim.x >> 6;
+  const int nblk = K / 32;
+  const int j = wave * 64 + lane;
+  const bool live = j < nblk;
+  const int g0 = (int)blockIdx.x * groups_per_wg;
+  const int groups_total = (N + kRows - 1) / kRows;
+  const int ng = groups_total - g0 < groups_per_wg ? groups_total - g0 : groups_per_wg;   // >= 1
+  const int row0 = g0 * kRows;
+  const int rows_here = N - row0 < ng * kRows ? N - row0 : ng * kRows;
+  const uint32_t row_bytes = (uint32_t)K * Q / 8;
+  const uint32_t groups_per_row = (uint32_t)K / G;
+  const uint32_t magic = kMagic;
+
+  // one descriptor per operand over the workgroup's rows: rows past N and blocks past
+  // the row read as zeros
+  const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + (int64_t)row0 * row_bytes, (uint32_t)rows_here * row_bytes);
+  const __amdgpu_buffer_rsrc_t rs =
+      make_rsrc(scales + (int64_t)row0 * groups_per_row, (uint32_t)rows_here * groups_per_row * 2);
+  const __amdgpu_buffer_rsrc_t rz =
+      make_rsrc(kMetaSize ? zp + (int64_t)row0 * groups_per_row * kMetaSize : zp,
+                kMetaSize ? (uint32_t)rows_here * groups_per_row * kMetaSize : 0u);
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
+
+  // The wavefront's 4 KB of activations: four contiguous 1 KB loads, then through a
+  // wavefront-private LDS area to the lane that owns each block (chunk c = 64 i + lane is
+  // piece c % 4 of block c / 4; chunks past K read zeros).
+  extern __shared__ u32x4 xstage[];
+  u32x4* const xw = xstage + wave * kXChunks;
+  u32x4 xq[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    xq[i] = __builtin_amdgcn_raw_buffer_load_b128(rx, wave * 4096 + 1024 * i + 16 * lane, 0, 0);
+  // A ring of D groups in registers: while group i is multiplied, groups i+1..i+D-1
+  // are in flight.  The run is unrolled at compile time (PER groups, groups past the
+  // workgroup's ng read zeros without touching memory: their rows lie past the
+  // descriptors), so every wait is for exactly the group about to be consumed; a loop
+  // or a data-dependent branch would make the compiler drain every load in flight.
+  StatGroup<Q> st[D];
+#pragma unroll
+  for (int d = 0; d < D - 1 && d < PER; ++d)
+    stat_issue<Q, G, META>(st[d], d, live, j, row_bytes, groups_per_row, rc, rs, rz);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) xw[x_slot(16 * i + (lane >> 2), lane & 3)] = xq[i];
+  wave_sync_lds();
+  uint32_t X[16];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const u32x4 v = xw[x_slot(lane, p)];
+    X[4 * p] = v.x; X[4 * p + 1] = v.y; X[4 * p + 2] = v.z; X[4 * p + 3] = v.w;
+  }
+  uint32_t xp[16];
+  float xs, xb;
+  block_x<Q>(X, xp, xs, xb);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    if (i + D - 1 < PER)
+      stat_issue<Q, G, META>(st[(i + D - 1) % D], i + D - 1, live, j, row_bytes, groups_per_row, rc, rs, rz);
+    const float v = stat_rows<Q, META>(st[i % D], xp, xs, xb, magic);
+    if (i < ng && (lane & 15) == 0) part[i][wave][fold4_row(lane)] = v;
+  }
+  __syncthreads();
+  for (int t = (int)threadIdx.x; t < rows_here; t += (int)blockDim.x) {
+    float v = 0.0f;
+    for (int w = 0; w < waves; ++w) v += part[t / kRows][w][t % kRows];
+    y[row0 + t] = f32_to_bf16_bits(v);
+  }
+}
+
+template <int Q, int G, int META, int PER>
+void gemv_stat_launch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales, const void* meta,
+                      int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+  const int64_t waves = (K / 32 + 63) / 64;
+  const int64_t groups = (N + kRows - 1) / kRows;
+  const dim3 grid((unsigned)((groups + PER - 1) / PER));
+  gemv_stat_kernel<Q, G, META, kStatDepth, PER><<<grid, (unsigned)(64 * waves), (size_t)waves * kXChunks * 16, stream>>>(
+      x, codes, scales, meta, (int)N, (int)K, PER, y);
+}
+
+// Runs of PER = 4 or 8 row groups per workgroup: 4 while that fits the matrix into one
+// round of resident workgroups, else 8.  Returns false (nothing launched) for matrices
+// that one round covers with runs of two groups or fewer: there every wavefront of the
+// pass-looping kernel has its loads in flight from the start, and that kernel measured
+// faster (its activation work per row is higher, but it runs twice the wavefronts).
+template <int Q, int G, int META>
+bool gemv_stat_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales, const void* meta,
+                        int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+  const int64_t waves = (K / 32 + 63) / 64;
+  if (waves > kStatMaxWaves) return false;
+  const int64_t groups = (N + kRows - 1) / kRows;
+  const int64_t slots = kCUs * std::max<int64_t>(1, kStatWavesPerCU / waves);
+  if (groups <= 2 * slots) return false;
+  if (groups <= 4 * slots) gemv_stat_launch<Q, G, META, 4>(x, codes, scales, meta, N, K, y, stream);
+  else gemv_stat_launch<Q, G, META, 8>(x, codes, scales, meta, N, K, y, stream);
+  return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -496,12 +688,21 @@ hipError_t f32_dispatch(const float* x, int64_t M, const uint8_t* codes, const u
   return hipGetLastError();
 }
 
+// One token: the activation-stationary kernel where it applies (gemv_stat_dispatch),
+// else the pass-looping kernel.
+template <int Q, int G, int META>
+hipError_t gemv1_dispatch(const uint16_t* x, const uint8_t* codes, const uint16_t* scales, const void* meta,
+                          int64_t N, int64_t K, uint16_t* y, hipStream_t stream) {
+  if (gemv_stat_dispatch<Q, G, META>(x, codes, scales, meta, N, K, y, stream)) return hipGetLastError();
+  return gemv_dispatch<Q, G, META>(x, codes, scales, meta, N, K, y, stream);
+}
+
 }  // namespace
 
 hipError_t launch_gemv_bf16(const uint16_t* x, const uint8_t* codes, const uint16_t* scales,
                             GroupMeta meta, int64_t N, int64_t K, int group, int q, uint16_t* y,
                             hipStream_t stream) {
-  SSQ_DISPATCH_QGM(gemv_dispatch, q, group, meta.kind, x, codes, scales, meta.ptr, N, K, y, stream);
+  SSQ_DISPATCH_QGM(gemv1_dispatch, q, group, meta.kind, x, codes, scales, meta.ptr, N, K, y, stream);
 }
 
 // Two tokens through one pass over the weights (M = 2).
