@@ -81,7 +81,7 @@ def measured_traffic(kind: str, mode: str = "signed_sym"):
     except (OSError, ValueError):
         return None
     entry = data.get(kind)
-    if not entry or entry.get("source_sha") != kernel_source_sha(KERNEL_SOURCES[kind]):
+    if not entry or entry.get("source_sha") != kernel_source_sha(KERNEL_SOURCES[kind.split(":")[0]]):
         return None
     return entry.get("hbm_bytes_per_launch")
 
@@ -141,6 +141,8 @@ def parse_args():
                         "gemv70b is the decode GEMV on the Llama3-70B down-projection "
                         "(8192x28672); 'copy' adds a plain 256 MiB device copy used to "
                         "calibrate byte counters")
+    p.add_argument("--quantize-copies", type=int, default=3,
+                   help="distinct weight matrices (and outputs) the quantize phase rotates over")
     p.add_argument("--layers70b", type=int, default=4,
                    help="distinct quantized copies of the 8192x28672 matrix (gemv70b phase)")
     return p.parse_args()
@@ -594,7 +596,11 @@ def main() -> int:
     layers = []
     for _ in range(args.layers):
         layers.append(ssq.ssq_quantize(W, g, q, mode))
-    staging = ssq.ssq_quantize(W, g, q, mode)                      # quantize target each step
+    # The quantize phase rotates over --quantize-copies copies of W and of its outputs
+    # (3 x 150 MB by default, past the 256 MB Infinity Cache), so each step streams its
+    # operands from HBM rather than from the cache a single re-quantized matrix would fit.
+    Wq = [W] + [W.clone() for _ in range(args.quantize_copies - 1)]
+    staging = [ssq.ssq_quantize(w_, g, q, mode) for w_ in Wq]
     y1 = torch.empty((1, N), dtype=torch.bfloat16, device=dev)
     ym = torch.empty((args.gemm_m, N), dtype=torch.bfloat16, device=dev)
     yb = torch.empty((args.batched_m, N), dtype=torch.bfloat16, device=dev)
@@ -676,7 +682,7 @@ def main() -> int:
         if ev:
             ev[0].record()
         if "quantize" in phases:
-            ssq.ssq_quantize(W, g, q, mode, out=staging)
+            ssq.ssq_quantize(Wq[i % len(Wq)], g, q, mode, out=staging[i % len(Wq)])
         if ev:
             ev[1].record()
         if "gemv" in graphs:
@@ -745,7 +751,7 @@ def main() -> int:
                    "group": g, "mode": args.mode, "decode_M": 1, "decode_layers": args.layers,
                    "prefill_M": args.gemm_m, "prefill_layers": args.gemm_layers,
                    "prefill_workspace_bytes": 0 if gemm_ws is None else gemm_ws.numel(),
-                   "batched_M": args.batched_m,
+                   "batched_M": args.batched_m, "quantize_copies": args.quantize_copies,
                    "batched_workspace_bytes": 0 if batched_ws is None else batched_ws.numel(),
                    "weights": f"bf16 Student-t(5)*0.02 + 0.1% x20 outliers, seed {spec.seed}"},
         "wall_s": round(wall, 4),
@@ -796,8 +802,8 @@ def main() -> int:
                                     "weights": f"bf16 Student-t(5)*0.015 + 0.1% x20 outliers, seed {s70.seed}"}
         out["roofline_gemv_70b"] = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
                                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                                    "traffic": None,
-                                    "kernel": f"gemv_kernel (ssq_matmul, M=1, {N70}x{K70})",
+                                    "traffic": measured_traffic("gemv:70b", args.mode),
+                                    "kernel": f"gemv_stat_kernel (ssq_matmul, M=1, {N70}x{K70})",
                                     "bytes_per_launch": b70, "avg_launch_us": round(avg * 1e6, 3)}
         out["roofline_gemv_70b"]["median_launch_us"], out["roofline_gemv_70b"]["cv"] = \
             spread(4, len(layers70))
