@@ -429,9 +429,11 @@ def sweep(args) -> int:
                          "frac_gain_gt_0_given_margin_gt_0": round(float(tally[2, 2]) / max(1, tally[2].sum()), 4)})
             del outs
 
-    # Q8_0 activations + integer-dot decode GEMV (App. C, App. B.3) against the bf16
-    # GEMV on the same quantized copies of the block (M = 1, graph-timed), per q and
-    # layout; the activation quantization is timed separately (one launch per K).
+    # Q8_0 activations + integer-dot matmul (App. C, App. B.3) against the bf16 path on
+    # the same quantized copies of the block (graph-timed), per q and layout: decode
+    # (M = 1, the one-token kernel) and batched decode (M = 16, integer MFMA against the
+    # bf16 MFMA kernel with its split workspace); the activation quantization is timed
+    # separately (one launch per K).
     for q in (2, 3, 4) if "q8" in parts else ():
         for mode_name in ("signed_sym", "asym", "asym_min"):
             mode = ssq.MODES[mode_name]
@@ -440,35 +442,38 @@ def sweep(args) -> int:
             wbytes = sum(matmul_bytes(0, N, K, q, 32, meta) for N, K in shapes.values())
             copies = [{n: ssq.ssq_quantize(W[n], 32, q, mode) for n in names}
                       for _ in range(max(1, -(-HBM_TARGET_BYTES // wbytes)))]
-            xs = {K: dev_bf16(synth.activations(1, K, seed=wl.x_seed + 1)) for _, K in shapes.values()}
-            acts = {K: ssq.ssq_quantize_act_q8(x) for K, x in xs.items()}
-            ys = {n: torch.empty((1, N), dtype=torch.bfloat16, device=dev) for n, (N, K) in shapes.items()}
+            for M in (1, 16):
+                xs = {K: dev_bf16(synth.activations(M, K, seed=wl.x_seed + M)) for _, K in shapes.values()}
+                acts = {K: ssq.ssq_quantize_act_q8(x) for K, x in xs.items()}
+                ys = {n: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for n, (N, K) in shapes.items()}
+                wss = {n: ssq.ssq_matmul_workspace(M, N, K, 32, q, device=dev) for n, (N, K) in shapes.items()}
 
-            def run_q8():
-                for c in copies:
-                    for n in names:
-                        N, K = shapes[n]
-                        ssq.ssq_matmul_q8(*acts[K], *c[n], N, K, 32, q, out=ys[n])
+                def run_q8():
+                    for c in copies:
+                        for n in names:
+                            N, K = shapes[n]
+                            ssq.ssq_matmul_q8(*acts[K], *c[n], N, K, 32, q, out=ys[n])
 
-            def run_bf16():
-                for c in copies:
-                    for n in names:
-                        N, K = shapes[n]
-                        ssq.ssq_matmul(xs[K], *c[n], N, K, 32, q, out=ys[n])
+                def run_bf16():
+                    for c in copies:
+                        for n in names:
+                            N, K = shapes[n]
+                            ssq.ssq_matmul(xs[K], *c[n], N, K, 32, q, out=ys[n], workspace=wss[n])
 
-            t_q8 = _graph_time(torch, run_q8, 10) / len(copies)
-            t_bf = _graph_time(torch, run_bf16, 10) / len(copies)
-            # 25 rounds per graph: a replay of a graph of two microsecond launches is bound
-            # by the host's graph launch, not by the kernels
-            t_act = _graph_time(torch, lambda: [ssq.ssq_quantize_act_q8(x, out=acts[K])
-                                                for _ in range(25) for K, x in xs.items()], 10) / 25
-            mb = sum(N * K * q // 8 + (2 + meta) * N * K // 32 + K + K // 16 + 2 * N for N, K in shapes.values())
-            rows.append({"block": wl.name, "op": "q8 gemv M=1", "q": q, "group": 32, "mode": mode_name,
-                         "launches": len(names), "copies": len(copies), "us": round(t_q8 * 1e6, 2),
-                         "bytes": mb, "gbs": round(mb / t_q8 / 1e9, 1),
-                         "frac_hbm": round(mb / t_q8 / 1e9 / HBM_PEAK_GBS, 4),
-                         "bf16_gemv_us": round(t_bf * 1e6, 2), "speedup_vs_bf16": round(t_bf / t_q8, 3),
-                         "act_quantize_us": round(t_act * 1e6, 2), "act_quantize_launches": len(xs)})
+                t_q8 = _graph_time(torch, run_q8, 10) / len(copies)
+                t_bf = _graph_time(torch, run_bf16, 10) / len(copies)
+                # 25 rounds per graph: a replay of a graph of two microsecond launches is
+                # bound by the host's graph launch, not by the kernels
+                t_act = _graph_time(torch, lambda: [ssq.ssq_quantize_act_q8(x, out=acts[K])
+                                                    for _ in range(25) for K, x in xs.items()], 10) / 25
+                mb = sum(N * K * q // 8 + (2 + meta) * N * K // 32 + M * (K + K // 16 + 2 * N)
+                         for N, K in shapes.values())
+                rows.append({"block": wl.name, "op": f"q8 matmul M={M}", "q": q, "group": 32, "mode": mode_name,
+                             "launches": len(names), "copies": len(copies), "us": round(t_q8 * 1e6, 2),
+                             "bytes": mb, "gbs": round(mb / t_q8 / 1e9, 1),
+                             "frac_hbm": round(mb / t_q8 / 1e9 / HBM_PEAK_GBS, 4),
+                             "bf16_us": round(t_bf * 1e6, 2), "speedup_vs_bf16": round(t_bf / t_q8, 3),
+                             "act_quantize_us": round(t_act * 1e6, 2), "act_quantize_launches": len(xs)})
             del copies
             torch.cuda.empty_cache()
 

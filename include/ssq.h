@@ -306,8 +306,9 @@ int ssq_quantize_act_q8(const uint16_t* x, int64_t M, int64_t K, int8_t* q, uint
  *   I = sum_{j in b} qx[m, j] u[n, j],  R = sum_{j in b} qx[m, j]     (exact integers)
  *   y[m, n] += d[m, b] s[n, g] (I - o[n, g] R)
  * with o = 2^(q-1) (zp == NULL: the symmetric formats) or the zero point zp[n, g].
- * Integer 4-way byte dot products; fp32 accumulation; y rounded to bf16 once.
- * A decode kernel: each token streams the weights once (M = 1 is the target).
+ * Exact integer block terms (4-way byte dot products at M = 1; int8 MFMA, v_mfma_i32_16x16x32_i8,
+ * for 2 <= M, where up to 32 tokens share one read of the weights and K <= 32768; longer
+ * rows take the M = 1 kernel per token); fp32 accumulation; y rounded to bf16 once.
  *
  *   qx, dx codes and scales from ssq_quantize_act_q8 ([M, K] int8, 16-byte aligned;
  *          [M, K/32] binary16, 2-byte aligned)

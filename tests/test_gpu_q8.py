@@ -138,3 +138,54 @@ def test_q8_pipeline_llama3_8b_down_proj_full_size():
     assert np.array_equal(codes.cpu().numpy()[rows], r.codes)
     ref = O.matmul_q8(a.q, a.d, r.codes, r.scales, None, len(rows), spec.cols, 32, 4)
     assert_q8_close(y, ref, rows, "q8 pipeline down_proj")
+
+
+# ---------------------------------------------------------------------------
+# Batched decode (2 <= M <= 32 per launch, integer MFMA, one read of the weights).
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M", [2, 16, 17, 32, 33, 40])
+@pytest.mark.parametrize("mode", MODES)
+def test_matmul_q8_batched_token_counts(M, mode):
+    """One and two 16-token tiles, and more than 32 tokens (launches of 32 and the rest);
+    70 rows (a ragged last 16-row workgroup) and K = 2016 (63 blocks: a ragged last quad)."""
+    rng = np.random.default_rng(M * 5 + mode)
+    w = O.bf16_bits_to_f32(bf16_bits(rng.standard_t(5, size=(70, 2016)) * 0.02))
+    check_q8_matmul(w, act_bits(M, 2016, seed=M + 100), 32, 4, mode, tag=f"batched M={M} m={mode}")
+
+
+@pytest.mark.parametrize("q", [2, 3, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+def test_matmul_q8_batched_formats(q, group):
+    """Every q and group size at M = 16 with K = 4224 (33 quads over 16 wavefronts)."""
+    rng = np.random.default_rng(q * 13 + group)
+    w = O.bf16_bits_to_f32(bf16_bits(rng.standard_t(5, size=(33, 4224)) * 0.02))
+    for mode in MODES:
+        check_q8_matmul(w, act_bits(16, 4224, seed=q + group + mode), group, q, mode,
+                        tag=f"batched q={q} g={group} m={mode}")
+
+
+def test_matmul_q8_batched_long_rows_fall_back():
+    """K past the batched kernel's token-scale staging (K > 32768) takes the one-token
+    kernel per token; same answers."""
+    rng = np.random.default_rng(77)
+    w = O.bf16_bits_to_f32(bf16_bits(rng.standard_t(5, size=(9, 33792)) * 0.02))
+    check_q8_matmul(w, act_bits(3, 33792, seed=78), 32, 4, O.SIGNED_SYM, tag="batched K=33792")
+
+
+@pytest.mark.parametrize("M", [16, 32])
+def test_q8_batched_llama3_8b_down_proj_full_size(M):
+    """4096x14336 at W4 g32, signed, M tokens through one read of the weights, sampled rows."""
+    spec = synth.llama3_8b_decode().layers["down_proj"]
+    wb = synth.weights(spec)
+    x = act_bits(M, spec.cols, seed=31 + M, scale=0.5)
+    codes, scales, zp = ssq.ssq_quantize(to_device(wb, True), 32, 4, O.SIGNED_SYM)
+    qx, dx, a = check_act(x, tag="batched activations")
+    g_y = Guarded((M, spec.rows), torch.bfloat16)
+    ssq.ssq_matmul_q8(qx, dx, codes, scales, zp, spec.rows, spec.cols, 32, 4, out=g_y.t)
+    g_y.check("batched full size")
+    rows = sample_rows(spec.rows, 64, seed=M)
+    r = O.quantize(O.bf16_bits_to_f32(wb[rows]), 32, 4, O.SIGNED_SYM)
+    assert np.array_equal(codes.cpu().numpy()[rows], r.codes)
+    ref = O.matmul_q8(a.q, a.d, r.codes, r.scales, None, len(rows), spec.cols, 32, 4)
+    assert_q8_close(g_y.t, ref, rows, f"q8 batched down_proj M={M}")
