@@ -84,6 +84,14 @@ READINGS = {
                  "(fp16 minimum), each block term exact in binary64 and the sum over blocks in "
                  "binary64.",
     "bit_order": "Field k of a row occupies bits [k*q, k*q+q) of the row's little-endian bit stream.",
+    "gguf_order": "App. B.1's formats table fixes the GGUF block fields and sizes (binary16 s, for "
+                  "Q*_1 a binary16 m, then qs; 18/20 bytes at q=4, 10/12 at q=2), not the index "
+                  "order inside qs.  Q4 follows the 4-bit unpack the paper names (one shift and "
+                  "one mask give indices 0..15 and 16..31): byte j = u[j] | u[j+16] << 4.  Q2 "
+                  "follows the described 2-bit unpack (four shift-and extractions, then byte and "
+                  "word interleaves restore element order): byte i = u[4i] | u[4i+1] << 2 | "
+                  "u[4i+2] << 4 | u[4i+3] << 6.  Binary16 fields are little-endian.  With a "
+                  "group of 64 or 128 each 32-weight block repeats its group's s (and m).",
 }
 
 
@@ -420,3 +428,65 @@ def matmul_q8(qx: np.ndarray, dx: np.ndarray, codes: np.ndarray, scales: np.ndar
              else np.repeat(np.asarray(zp, np.int64).reshape(N, K // group), per, axis=1))
         term = s[None] * (I - o[None] * R[:, None, :]).astype(np.float64)
     return (d[:, None, :] * term).sum(axis=-1)
+
+
+# ---------------------------------------------------------------------------
+# App. B.1 (formats table): llama.cpp GGUF blocks, array of structures.
+# ---------------------------------------------------------------------------
+
+def gguf_block_bytes(q: int, with_min: bool) -> int:
+    """Bytes of one 32-weight block: binary16 s, [binary16 m,] 32 q-bit indices."""
+    return 2 + (2 if with_min else 0) + 32 * q // 8
+
+
+def to_gguf(u: np.ndarray, scales: np.ndarray, mins: Optional[np.ndarray], group: int, q: int) -> np.ndarray:
+    """GGUF blocks of indices u [rows, cols] (cols a multiple of 32) with binary16 scales
+    (and minimums) [rows, cols/group]: uint8 [rows, cols/32, gguf_block_bytes(q, ...)].
+    Index order inside qs: READINGS["gguf_order"]."""
+    u = np.asarray(u, dtype=np.int64)
+    rows, cols = u.shape
+    nb = cols // 32
+    ub = u.reshape(rows, nb, 32)
+    if q == 4:
+        qs = ub[:, :, :16] | (ub[:, :, 16:] << 4)                                 # [rows, nb, 16]
+    elif q == 2:
+        quads = ub.reshape(rows, nb, 8, 4)
+        qs = quads[..., 0] | (quads[..., 1] << 2) | (quads[..., 2] << 4) | (quads[..., 3] << 6)
+    else:
+        raise ValueError("GGUF blocks exist for q = 2 and q = 4 only")
+    per = group // 32
+    fields = [np.repeat(np.asarray(scales, np.uint16).reshape(rows, cols // group), per, axis=1)]
+    if mins is not None:
+        fields.append(np.repeat(np.asarray(mins, np.uint16).reshape(rows, cols // group), per, axis=1))
+    parts = []
+    for f in fields:                                         # binary16, little-endian
+        parts += [(f & 0xFF)[..., None], (f >> 8)[..., None]]
+    parts.append(qs)
+    return np.concatenate(parts, axis=-1).astype(np.uint8)
+
+
+def from_gguf(blocks: np.ndarray, q: int, with_min: bool):
+    """Inverse of :func:`to_gguf` at group 32: (u int64 [rows, cols], s uint16 [rows, cols/32],
+    m uint16 [rows, cols/32] or None)."""
+    b = np.asarray(blocks, dtype=np.uint16)
+    rows, nb, _ = b.shape
+    s = b[..., 0] | (b[..., 1] << 8)
+    m = (b[..., 2] | (b[..., 3] << 8)) if with_min else None
+    qs = b[..., 4 if with_min else 2:].astype(np.int64)
+    if q == 4:
+        u = np.concatenate([qs & 0xF, qs >> 4], axis=-1)                        # [rows, nb, 32]
+    else:
+        u = np.stack([(qs >> (2 * k)) & 3 for k in range(4)], axis=-1).reshape(rows, nb, 32)
+    return u.reshape(rows, nb * 32), s, m
+
+
+def gguf_dequantize(blocks: np.ndarray, q: int, with_min: bool) -> np.ndarray:
+    """Weights in binary64 as the formats read back: s*(u - 2^(q-1)) for Q*_0 (Q*_0s),
+    s*u + m for Q*_1."""
+    u, s, m = from_gguf(blocks, q, with_min)
+    rows, cols = u.shape
+    sb = f16_bits_to_f64(s).reshape(rows, cols // 32, 1)
+    ub = u.reshape(rows, cols // 32, 32).astype(np.float64)
+    if with_min:
+        return (sb * ub + f16_bits_to_f64(m).reshape(rows, cols // 32, 1)).reshape(rows, cols)
+    return (sb * (ub - (1 << (q - 1)))).reshape(rows, cols)

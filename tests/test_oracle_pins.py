@@ -745,3 +745,42 @@ def test_matmul_q8_equals_matmul_on_dequantized_activations():
         y = O.matmul_q8(a.q, a.d, r.codes, r.scales, r.zp, 40, 512, 32, 4, mins=r.mins)
         ref = O.matmul(xh, r.codes, r.scales, r.zp, 40, 512, 32, 4, mins=r.mins)
         assert np.allclose(y, ref, rtol=1e-12, atol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# App. B.1 formats table: GGUF array-of-structures blocks.
+# ---------------------------------------------------------------------------
+
+def test_gguf_blocks_match_hand_derived_bytes(golden_dir):
+    """Three blocks whose bytes were derived by hand from the formats table (fixture),
+    including a negative (signed-symmetric) scale; sizes as the table."""
+    gold = json.load(open(os.path.join(golden_dir, "gguf_blocks.json")))
+    sizes = json.load(open(os.path.join(golden_dir, "paper_block_sizes.json")))
+    for c in gold["cases"]:
+        u = np.array([c["u"]])
+        s = np.array([[int(c["s_f16"], 16)]], np.uint16)
+        m = np.array([[int(c["m_f16"], 16)]], np.uint16) if c["with_min"] else None
+        b = O.to_gguf(u, s, m, 32, c["q"])
+        assert b.shape == (1, 1, O.gguf_block_bytes(c["q"], c["with_min"]))
+        assert b.shape[-1] == sizes[f"Q{c['q']}_{1 if c['with_min'] else 0}"]
+        assert b[0, 0].tobytes().hex() == c["hex"], c["format"]
+        u2, s2, m2 = O.from_gguf(b, c["q"], c["with_min"])
+        assert np.array_equal(u2, u) and np.array_equal(s2, s)
+        np.testing.assert_array_equal(O.gguf_dequantize(b, c["q"], c["with_min"])[0, :4], c["weights_first4"])
+
+
+@pytest.mark.parametrize("q", [2, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("mode", [SIGNED, UNSIGNED, ASYM_MIN])
+def test_gguf_round_trip_reads_back_the_same_weights(q, group, mode):
+    """Blocks decoded byte by byte give the weights the packed bit stream gives (two
+    independent decodings: App. B.1 blocks against App. B.3's dequantization)."""
+    w = f32_groups(13, 256, q * 100 + group + mode)
+    r = O.quantize(w, group, q, mode)
+    b = O.to_gguf(r.u, r.scales, r.mins, group, q)
+    assert b.shape == (13, 256 // 32, O.gguf_block_bytes(q, r.mins is not None))
+    expect = O.dequantize(r.codes, r.scales, r.zp, 256, group, q, r.mins)
+    got = O.gguf_dequantize(b, q, r.mins is not None)
+    assert np.array_equal(got, expect)
+    u, s, m = O.from_gguf(b, q, r.mins is not None)
+    assert np.array_equal(u, O.unpack(r.codes, 256, q))
