@@ -325,6 +325,35 @@ int ssq_matmul_q8_min(const int8_t* qx, const uint16_t* dx, int64_t M, const uin
                       const uint16_t* scales, const uint16_t* mins, int64_t N, int64_t K, int group,
                       int q, uint16_t* y, hipStream_t stream);
 
+/*
+ * ssq_export_gguf -- the packed weights as llama.cpp GGUF blocks (App. B.1, formats
+ * table; App. B.2 notes that quantized models can be exported to that runtime).  Per 32
+ * weights of a row, one array-of-structures block: binary16 s, then (mins != NULL) a
+ * binary16 m, then the block's indices qs:
+ *   q = 4: Q4_0 / Q4_0s 18 bytes {s, qs[16]};  with mins Q4_1 20 bytes {s, m, qs[16]}
+ *   q = 2: Q2_0 / Q2_0s 10 bytes {s, qs[8]};   with mins Q2_1 12 bytes {s, m, qs[8]}
+ * The signed-symmetric variant (Q*_0s) is the Q*_0 layout with a scale that may be
+ * negative.  qs order: q = 4 byte j = index j | index (j+16) << 4 (j < 16); q = 2
+ * byte i = indices 4i..4i+3 at bits 0, 2, 4, 6.  A weight reads back as s*(u - 2^(q-1))
+ * (Q*_0) or s*u + m (Q*_1), as in this library.  With group 64 or 128 every 32-weight
+ * block repeats its group's s (and m).  Blocks are row-major: row r's blocks first.
+ *
+ *   codes, scales, mins  device, as ssq_quantize (SSQ_SIGNED_SYM or SSQ_UNSIGNED_SYM)
+ *                        or ssq_quantize_min wrote them; mins NULL for the symmetric
+ *                        formats.  The zero-point layout (SSQ_ASYM) has no GGUF form.
+ *   rows, cols, group, q q in {2, 4} (GGUF has no 3-bit block in the table)
+ *   blocks               device, written: rows * cols/32 * ssq_gguf_block_bytes(q, mins
+ *                        != NULL) bytes (2-byte aligned; codes 16, scales and mins 2)
+ *   stream               HIP stream
+ * Returns SSQ_OK, SSQ_EINVAL (q = 3, bad sizes, missing pointer) or SSQ_EALIGN.
+ */
+int ssq_export_gguf(const uint8_t* codes, const uint16_t* scales, const uint16_t* mins, int64_t rows,
+                    int64_t cols, int group, int q, uint8_t* blocks, hipStream_t stream);
+
+/* Bytes of one GGUF block of ssq_export_gguf: 18, 20 (q = 4), 10, 12 (q = 2) without and
+ * with a minimum; 0 for any other q. */
+int64_t ssq_gguf_block_bytes(int q, int with_min);
+
 /* Static description of a status code; never NULL. */
 const char* ssq_strerror(int status);
 

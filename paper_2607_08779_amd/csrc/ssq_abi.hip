@@ -324,6 +324,21 @@ int ssq_matmul_q8_min(const int8_t* qx, const uint16_t* dx, int64_t M, const uin
   return status_of(ssq::launch_matmul_q8(qx, dx, M, codes, scales, minimums(mins), N, K, group, q, y, stream));
 }
 
+int64_t ssq_gguf_block_bytes(int q, int with_min) {
+  return q == 2 || q == 4 ? ssq::gguf_block_bytes(q, with_min != 0) : 0;
+}
+
+int ssq_export_gguf(const uint8_t* codes, const uint16_t* scales, const uint16_t* mins, int64_t rows,
+                    int64_t cols, int group, int q, uint8_t* blocks, hipStream_t stream) {
+  if (rows < 0 || cols < 0 || rows > kMaxDim || cols > kMaxDim || rows * cols > kMaxElems) return SSQ_EINVAL;
+  if ((q != 2 && q != 4) || !valid_group(group) || cols % group != 0) return SSQ_EINVAL;
+  if (rows == 0 || cols == 0) return SSQ_OK;
+  if (codes == nullptr || scales == nullptr || blocks == nullptr) return SSQ_EINVAL;
+  if (!aligned(codes, 16) || !aligned(scales, 2) || !aligned(blocks, 2) || (mins != nullptr && !aligned(mins, 2)))
+    return SSQ_EALIGN;
+  return status_of(ssq::launch_export_gguf(codes, scales, mins, rows, cols, group, q, blocks, stream));
+}
+
 const char* ssq_strerror(int status) {
   switch (status) {
     case SSQ_OK: return "success";

@@ -240,4 +240,9 @@ hipError_t launch_matmul_q8(const int8_t* qx, const uint16_t* dx, int64_t M, con
                             const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K, int group, int q,
                             uint16_t* y, hipStream_t stream);
 
+// GGUF array-of-structures export (export.hip): q in {2, 4}; mins null for Q*_0.
+int64_t gguf_block_bytes(int q, bool with_min);
+hipError_t launch_export_gguf(const uint8_t* codes, const uint16_t* scales, const uint16_t* mins, int64_t rows,
+                              int64_t cols, int group, int q, uint8_t* out, hipStream_t stream);
+
 }  // namespace ssq

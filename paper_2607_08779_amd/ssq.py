@@ -57,6 +57,10 @@ _EXPORTS["ssq_quantize_act_q8"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int6
                                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p])
 _EXPORTS["ssq_matmul_q8"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p] + _EXPORTS["ssq_matmul"][1][1:])
 _EXPORTS["ssq_matmul_q8_min"] = _EXPORTS["ssq_matmul_q8"]
+_EXPORTS["ssq_export_gguf"] = (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                              ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                              ctypes.c_void_p])
+_EXPORTS["ssq_gguf_block_bytes"] = (ctypes.c_int64, [ctypes.c_int, ctypes.c_int])
 
 _lib: Optional[ctypes.CDLL] = None
 
@@ -303,6 +307,20 @@ def ssq_matmul_q8(qx: torch.Tensor, dx: torch.Tensor, codes: torch.Tensor, scale
                             _ptr(y), _stream(qx.device))
     _check(fn, st)
     return y
+
+
+def ssq_export_gguf(codes: torch.Tensor, scales: torch.Tensor, mins: Optional[torch.Tensor], rows: int,
+                    cols: int, group: int, q: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The packed weights as GGUF blocks (uint8 [rows, cols/32, block bytes]: Q4_0/Q4_0s,
+    Q4_1, Q2_0/Q2_0s or Q2_1 by q and whether ``mins`` is given), on the current stream."""
+    if mins is not None and mins.dtype != torch.int16:
+        raise TypeError("mins must be int16 binary16 minimums (ssq_quantize_min)")
+    nbytes = int(lib().ssq_gguf_block_bytes(q, int(mins is not None)))
+    if out is None:
+        out = torch.empty((rows, cols // 32, max(nbytes, 1)), dtype=torch.uint8, device=codes.device)
+    _check("ssq_export_gguf", lib().ssq_export_gguf(_ptr(codes), _ptr(scales), _ptr(mins), rows, cols, group, q,
+                                                    _ptr(out), _stream(codes.device)))
+    return out
 
 
 def ssq_quantize_diag(W: torch.Tensor, group: int, q: int):

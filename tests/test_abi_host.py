@@ -24,7 +24,8 @@ def declared_functions():
 
 
 def test_header_declares_the_boundary():
-    assert declared_functions() == ["ssq_matmul", "ssq_matmul_f32", "ssq_matmul_min",
+    assert declared_functions() == ["ssq_export_gguf", "ssq_gguf_block_bytes",
+                                    "ssq_matmul", "ssq_matmul_f32", "ssq_matmul_min",
                                     "ssq_matmul_min_f32", "ssq_matmul_min_ws",
                                     "ssq_matmul_noalloc", "ssq_matmul_q8", "ssq_matmul_q8_min",
                                     "ssq_matmul_workspace_size", "ssq_matmul_ws",
@@ -256,3 +257,24 @@ def test_quantize_diag_rejects_invalid_arguments(args, status):
     for fn in (ssq.lib().ssq_quantize_diag, ssq.lib().ssq_quantize_diag_f32):
         assert fn(a["W"], a["rows"], a["cols"], a["group"], a["q"], a["codes"], a["scales"], a["margin"],
                   a["gain"]) == status
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(q=3), EINVAL), (dict(q=5), EINVAL), (dict(group=16), EINVAL), (dict(cols=48), EINVAL),
+    (dict(rows=-1), EINVAL), (dict(codes=None), EINVAL), (dict(scales=None), EINVAL), (dict(out=None), EINVAL),
+    (dict(codes=P2), EALIGN), (dict(scales=ctypes.c_void_p((1 << 20) + 1)), EALIGN),
+    (dict(out=ctypes.c_void_p((1 << 20) + 1)), EALIGN), (dict(mins=ctypes.c_void_p((1 << 20) + 1)), EALIGN),
+])
+def test_export_gguf_rejects_invalid_arguments(args, status):
+    a = dict(codes=P16, scales=P16, mins=None, rows=4, cols=64, group=32, q=4, out=P16)
+    a.update(args)
+    assert ssq.lib().ssq_export_gguf(a["codes"], a["scales"], a["mins"], a["rows"], a["cols"], a["group"],
+                                     a["q"], a["out"], None) == status
+
+
+def test_export_gguf_block_sizes_and_empty():
+    """Block sizes of App. B.1's formats table; an empty matrix is a no-op."""
+    lib = ssq.lib()
+    assert [lib.ssq_gguf_block_bytes(q, m) for q in (4, 2) for m in (0, 1)] == [18, 20, 10, 12]
+    assert lib.ssq_gguf_block_bytes(3, 0) == 0
+    assert lib.ssq_export_gguf(None, None, None, 0, 64, 32, 4, None, None) == 0
