@@ -468,22 +468,52 @@ struct StatGroup {
   uint32_t z[kRows];
 };
 
-// Loads of row group i of the workgroup (rows 4i..4i+3 of its run) for block j.
+// A lane's load offsets for its block j in the four rows of a group, the same for every
+// group (each group gets descriptors of its own, see stat_rsrc); past the row's blocks
+// they point out of range.
+struct StatOffsets {
+  uint32_t c[kRows], s[kRows], z[kRows];
+};
+
 template <int Q, int G, int META>
-__device__ __forceinline__ void stat_issue(StatGroup<Q>& st, int i, bool live, int j, uint32_t row_bytes,
-                                           uint32_t groups_per_row, __amdgpu_buffer_rsrc_t rc,
-                                           __amdgpu_buffer_rsrc_t rs, __amdgpu_buffer_rsrc_t rz) {
-  constexpr int kBlocksPerGroup = G / 32;
-  const uint32_t g = (uint32_t)(j / kBlocksPerGroup);
+__device__ __forceinline__ StatOffsets stat_offsets(bool live, int j, uint32_t row_bytes, uint32_t groups_per_row) {
+  constexpr int kMetaSize = META == kMetaZp ? 1 : META == kMetaMin ? 2 : 0;
+  const uint32_t g = (uint32_t)(j / (G / 32));
+  StatOffsets o;
 #pragma unroll
   for (int r = 0; r < kRows; ++r) {
-    const uint32_t row = (uint32_t)(4 * i + r);
-    buffer_block_codes<Q>(rc, live ? row * row_bytes + (uint32_t)j * (4 * Q) : kOutOfRange, 0, st.cb[r].d);
-    st.s[r] = __builtin_amdgcn_raw_buffer_load_b16(rs, live ? (row * groups_per_row + g) * 2 : kOutOfRange, 0, 0);
+    o.c[r] = live ? (uint32_t)r * row_bytes + (uint32_t)j * (4 * Q) : kOutOfRange;
+    o.s[r] = live ? ((uint32_t)r * groups_per_row + g) * 2 : kOutOfRange;
+    o.z[r] = live ? ((uint32_t)r * groups_per_row + g) * kMetaSize : kOutOfRange;
+  }
+  return o;
+}
+
+// Descriptor over rows 4i.. of the workgroup's run (rows_here rows from `base`, `stride`
+// bytes each): scalar arithmetic only; groups past the run get an empty range.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t stat_rsrc(const void* base, uint32_t stride, int i, int rows_here) {
+  const int left = rows_here - 4 * i;
+  return make_rsrc(static_cast<const uint8_t*>(base) + (int64_t)(4 * i) * stride, left > 0 ? (uint32_t)left * stride : 0u);
+}
+
+// Loads of row group i of the workgroup's run (rows 4i..4i+3).
+template <int Q, int G, int META>
+__device__ __forceinline__ void stat_issue(StatGroup<Q>& st, int i, const StatOffsets& o, int rows_here,
+                                           uint32_t row_bytes, uint32_t groups_per_row, const uint8_t* cbase,
+                                           const uint16_t* sbase, const uint8_t* zbase) {
+  constexpr int kMetaSize = META == kMetaZp ? 1 : META == kMetaMin ? 2 : 0;
+  const __amdgpu_buffer_rsrc_t rc = stat_rsrc(cbase, row_bytes, i, rows_here);
+  const __amdgpu_buffer_rsrc_t rs = stat_rsrc(sbase, groups_per_row * 2, i, rows_here);
+  const __amdgpu_buffer_rsrc_t rz = stat_rsrc(zbase, kMetaSize ? groups_per_row * kMetaSize : 0u, i,
+                                              kMetaSize ? rows_here : 0);
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    buffer_block_codes<Q>(rc, o.c[r], 0, st.cb[r].d);
+    st.s[r] = __builtin_amdgcn_raw_buffer_load_b16(rs, o.s[r], 0, 0);
     if constexpr (META == kMetaMin)
-      st.z[r] = __builtin_amdgcn_raw_buffer_load_b16(rz, live ? (row * groups_per_row + g) * 2 : kOutOfRange, 0, 0);
+      st.z[r] = __builtin_amdgcn_raw_buffer_load_b16(rz, o.z[r], 0, 0);
     else if constexpr (META == kMetaZp)
-      st.z[r] = __builtin_amdgcn_raw_buffer_load_b8(rz, live ? row * groups_per_row + g : kOutOfRange, 0, 0);
+      st.z[r] = __builtin_amdgcn_raw_buffer_load_b8(rz, o.z[r], 0, 0);
     else
       st.z[r] = 0u;
   }
@@ -525,14 +555,12 @@ __global__ __launch_bounds__(1024) void gemv_stat_kernel(const uint16_t* __restr
   const uint32_t groups_per_row = (uint32_t)K / G;
   const uint32_t magic = kMagic;
 
-  // one descriptor per operand over the workgroup's rows: rows past N and blocks past
-  // the row read as zeros
-  const __amdgpu_buffer_rsrc_t rc = make_rsrc(codes + (int64_t)row0 * row_bytes, (uint32_t)rows_here * row_bytes);
-  const __amdgpu_buffer_rsrc_t rs =
-      make_rsrc(scales + (int64_t)row0 * groups_per_row, (uint32_t)rows_here * groups_per_row * 2);
-  const __amdgpu_buffer_rsrc_t rz =
-      make_rsrc(kMetaSize ? zp + (int64_t)row0 * groups_per_row * kMetaSize : zp,
-                kMetaSize ? (uint32_t)rows_here * groups_per_row * kMetaSize : 0u);
+  // the run's operands; each group's loads go through descriptors over its own rows, so
+  // rows past N and blocks past the row read as zeros and the offsets stay constant
+  const uint8_t* const cbase = codes + (int64_t)row0 * row_bytes;
+  const uint16_t* const sbase = scales + (int64_t)row0 * groups_per_row;
+  const uint8_t* const zbase = kMetaSize ? zp + (int64_t)row0 * groups_per_row * kMetaSize : zp;
+  const StatOffsets off = stat_offsets<Q, G, META>(live, j, row_bytes, groups_per_row);
   const __amdgpu_buffer_rsrc_t rx = make_rsrc(x, (uint32_t)K * 2);
 
   // The wavefront's 4 KB of activations: four contiguous 1 KB loads, then through a
@@ -552,7 +580,7 @@ __global__ __launch_bounds__(1024) void gemv_stat_kernel(const uint16_t* __restr
   StatGroup<Q> st[D];
 #pragma unroll
   for (int d = 0; d < D - 1 && d < PER; ++d)
-    stat_issue<Q, G, META>(st[d], d, live, j, row_bytes, groups_per_row, rc, rs, rz);
+    stat_issue<Q, G, META>(st[d], d, off, rows_here, row_bytes, groups_per_row, cbase, sbase, zbase);
 #pragma unroll
   for (int i = 0; i < 4; ++i) xw[x_slot(16 * i + (lane >> 2), lane & 3)] = xq[i];
   wave_sync_lds();
@@ -568,7 +596,8 @@ __global__ __launch_bounds__(1024) void gemv_stat_kernel(const uint16_t* __restr
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     if (i + D - 1 < PER)
-      stat_issue<Q, G, META>(st[(i + D - 1) % D], i + D - 1, live, j, row_bytes, groups_per_row, rc, rs, rz);
+      stat_issue<Q, G, META>(st[(i + D - 1) % D], i + D - 1, off, rows_here, row_bytes, groups_per_row, cbase,
+                             sbase, zbase);
     const float v = stat_rows<Q, META>(st[i % D], xp, xs, xb, magic);
     if (i < ng && (lane & 15) == 0) part[i][wave][fold4_row(lane)] = v;
   }
