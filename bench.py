@@ -246,6 +246,10 @@ HBM_TARGET_BYTES = 600 << 20    # distinct weight bytes per timed pass: over twi
 def _graph_time(torch, fn, reps: int) -> float:
     """Seconds per replay of a HIP graph holding the launches fn() makes."""
     s = torch.cuda.Stream()
+    # the side stream starts after the work queued so far (the inputs' producers): an
+    # unordered start could let fn()'s output writes land on memory the caller's stream
+    # is still reading, e.g. a temporary it freed
+    s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
         fn()
         torch.cuda.synchronize()
@@ -317,6 +321,7 @@ def stream_ceiling(torch, dev, nbytes: int, copies: int, reps: int):
     bufs = [torch.full((nbytes // 4,), i + 1, dtype=torch.int32, device=dev) for i in range(copies)]
     sink = torch.zeros(max(1, lib.ssq_bench_stream_read_sink_words(nbytes)), dtype=torch.int32, device=dev)
     s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
         def run():
             for b in bufs:
@@ -782,7 +787,8 @@ def main() -> int:
         out["roofline_batched"] = {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS,
                                    "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                                    "traffic": measured_traffic("batched", args.mode),
-                                   "kernel": f"skinny_split_kernel (ssq_matmul, M={args.batched_m})",
+                                   "kernel": ("skinny_stat_kernel" if args.batched_m <= 16 and q in (2, 4) and K % 512 == 0
+                                              else "skinny_split_kernel") + f" (ssq_matmul, M={args.batched_m})",
                                    "bytes_per_launch": batched_bytes, "avg_launch_us": round(avg * 1e6, 3),
                                    "tflops": round(2 * args.batched_m * N * K / avg / 1e12, 2)}
         out["roofline_batched"]["median_launch_us"], out["roofline_batched"]["cv"] = spread(2, args.layers)

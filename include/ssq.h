@@ -116,9 +116,12 @@ int ssq_quantize_f32(const float* W, int64_t rows, int64_t cols, int group, int 
  *   lives in the scale, so both run the same kernel), o = zp[n, b] otherwise.
  * Products accumulate in fp32; y is rounded to bf16 (half to even).
  * M = 1 and M = 2 run a streaming GEMV (two tokens share each unpacked block);
- * 3 <= M <= 32 (batched decode) dequantizes each weight once into bf16 MFMA
- * operands shared by all tokens; larger M runs a tiled
- * kernel that dequantizes weight tiles into LDS and multiplies them with bf16 MFMA.
+ * 3 <= M <= 32 (batched decode) shares each weight among the tokens through bf16
+ * MFMA: for q = 2 or 4, M <= 16 and K a multiple of 512 (with a workspace, or
+ * K <= 2048) the weights enter exactly (the code as 128 + u, the scale and offset
+ * applied per 32-weight block in fp32), otherwise each weight is dequantized once
+ * and rounded to bf16; larger M runs a tiled kernel that dequantizes weight tiles
+ * into LDS and multiplies them with bf16 MFMA.
  *
  *   x      device, bf16 bits [M, K] row-major, read only
  *   M      >= 0, number of activation rows (tokens)

@@ -211,7 +211,7 @@ int ssq_matmul_min(const uint16_t* x, int64_t M, const uint8_t* codes, const uin
 
 size_t ssq_matmul_workspace_size(int64_t M, int64_t N, int64_t K, int group, int q) {
   if (check_matmul_sizes(M, N, K, group, q) != SSQ_OK || M <= 2 || N == 0) return 0;   // GEMV: no split
-  return M <= ssq::kSkinnyMaxM ? ssq::skinny_workspace_bytes(M, N, K) : ssq::gemm_workspace_bytes(M, N, K);
+  return M <= ssq::kSkinnyMaxM ? ssq::skinny_workspace_bytes(M, N, K, q) : ssq::gemm_workspace_bytes(M, N, K);
 }
 
 int ssq_matmul_ws(const uint16_t* x, int64_t M, const uint8_t* codes, const uint16_t* scales,

@@ -217,7 +217,7 @@ hipError_t launch_skinny_bf16(const uint16_t* x, int64_t M, const uint8_t* codes
                               const uint16_t* scales, GroupMeta meta, int64_t N, int64_t K,
                               int group, int q, uint16_t* y, void* workspace, size_t workspace_bytes,
                               hipStream_t stream);
-size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K);
+size_t skinny_workspace_bytes(int64_t M, int64_t N, int64_t K, int q);
 
 // Sign-rule diagnostics (Sec. 4): per-group margin and gain, optional 3x3 tally.
 hipError_t launch_diagnostics_bf16(const uint16_t* W, int64_t rows, int64_t cols, int group, int q,

@@ -37,12 +37,24 @@ def quantize_guarded(W, rows, cols, group, q, mode, tag=""):
     return out
 
 
-def compare_matmul(y, x_real, ref_q, sel, K, group, q, bf16_x, tag):
+def exact_weight_path(M, K, q, workspace):
+    """Whether ssq_matmul runs the activation-stationary batched-decode kernel: q = 2 or
+    4, 3 <= M <= 16, K a multiple of a wavefront's range of 512 weights and either a
+    workspace or at most four ranges (one slice of K).  It keeps every weight exact,
+    where the dequantizing MFMA kernels round s (u - o) to bf16, so it is held to the
+    exact-weight bound."""
+    if q not in (2, 4) or not 3 <= M <= 16:
+        return False
+    return K % 512 == 0 and (workspace or K <= 2048)
+
+
+def compare_matmul(y, x_real, ref_q, sel, K, group, q, bf16_x, tag, workspace=False):
     """Element-wise comparison of y[:, sel] (a GPU tensor) with the oracle; returns rel L2."""
     M = x_real.shape[0]
     y_ref = O.matmul(x_real, ref_q.codes, ref_q.scales, ref_q.zp, len(sel), K, group, q, mins=ref_q.mins)
     w_hat = O.dequantize(ref_q.codes, ref_q.scales, ref_q.zp, K, group, q, ref_q.mins)
-    rounded = bf16_x and M > 2                   # batched decode and prefill round W_hat to bf16
+    # batched decode and prefill round W_hat to bf16, except the activation-stationary kernel
+    rounded = bf16_x and M > 2 and not exact_weight_path(M, K, q, workspace)
     bound, S = matmul_error_bound(x_real, w_hat, y_ref, rounded, f32=not bf16_x)
     y_all = y_to_f64(y)
     assert not np.isnan(y_all).any(), f"{tag}: output elements left unwritten (NaN fill)"
@@ -90,7 +102,8 @@ def check_matmul(w_host, x_host, group, q, mode, rows_idx=None, bf16_w=True, bf1
         y.check(f"{tag} y (call {r})")
         if ws is not None:
             ws.check(f"{tag} workspace (call {r})")
-        err = compare_matmul(y.t, xr, ref_q, sel, K, group, q, bf16_x, f"{tag} (call {r})")
+        err = compare_matmul(y.t, xr, ref_q, sel, K, group, q, bf16_x, f"{tag} (call {r})",
+                             workspace=ws is not None)
     return err
 
 
@@ -266,6 +279,37 @@ def test_skinny_split_token_counts(M, group):
         check_matmul(w, x, group, 4, mode, tag=f"skinny split M={M}", workspace=True, repeat=2)
 
 
+# Activation-stationary batched decode (q = 2, 4; K a multiple of the wavefront range).
+
+@pytest.mark.parametrize("M", [5, 16])
+@pytest.mark.parametrize("q", [2, 4])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("mode", MODES)
+def test_stationary_all_formats(M, q, group, mode):
+    # N=45: three 16-row tiles, the last one partial.  K=2560: five 512-wide ranges, two
+    # slices of four wavefronts (the second with one live); two calls on one workspace
+    assert exact_weight_path(M, 2560, q, True)
+    w = rand_w(45, 2560, seed=100 + 7 * q + group + mode + M)
+    x = synth.activations(M, 2560, seed=q * group + M)
+    check_matmul(w, x, group, q, mode, tag=f"stationary {M}x45x2560", workspace=True, repeat=2)
+
+
+@pytest.mark.parametrize("q", [2, 4])
+@pytest.mark.parametrize("M,N,K,workspace", [
+    (16, 6400, 4096, True),     # two slices, 400 tiles: runs of two tiles
+    (9, 9600, 6144, True),      # three slices, 600 tiles: runs of four, the last one short
+    (13, 4100, 3072, True),     # a 4-row last tile and a tile past N in the last run
+    (16, 2000, 1024, False),    # one slice (two live wavefronts): no workspace, y per tile
+])
+def test_stationary_runs(q, M, N, K, workspace):
+    assert exact_weight_path(M, K, q, workspace)
+    w = rand_w(N, K, seed=N + K + q)
+    x = synth.activations(M, K, seed=M + q)
+    for mode in (O.SIGNED_SYM, O.ASYM_MIN):
+        check_matmul(w, x, 32, q, mode, rows_idx=sample_rows(N, n=48, seed=q), tag=f"stationary runs {M}x{N}x{K}",
+                     workspace=workspace, repeat=2 if workspace else 1, need_split=False)
+
+
 @pytest.mark.parametrize("M,N,K", [(96, 256, 8192), (300, 256, 8192), (16, 256, 8192)])
 def test_split_reduction_graph_replay(M, N, K):
     """The split kernels in a HIP graph: the arrival counters reset inside the kernel, so
@@ -279,7 +323,8 @@ def test_split_reduction_graph_replay(M, N, K):
     assert ws is not None
     y_eager = ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4, workspace=ws)
     ref_q = O.quantize(widen(w, True), 32, 4, O.SIGNED_SYM)
-    compare_matmul(y_eager, widen(x_host, True), ref_q, np.arange(N), K, 32, 4, True, f"graph split M={M}")
+    compare_matmul(y_eager, widen(x_host, True), ref_q, np.arange(N), K, 32, 4, True, f"graph split M={M}",
+                   workspace=True)
     y = torch.empty_like(y_eager)
     ssq.ssq_matmul(x, codes, scales, None, N, K, 32, 4, out=y, workspace=ws)
     torch.cuda.synchronize()
@@ -410,6 +455,19 @@ def test_prefill_headline_split_full_size():
     x = synth.activations(512, spec.cols, seed=wl.x_seed + 512)
     check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=32, seed=9),
                  tag="prefill down_proj M=512 split", workspace=True, repeat=2)
+
+
+@pytest.mark.parametrize("M", [16, 32])
+def test_llama3_8b_batched_decode_full_size(M):
+    """Batched decode through the split-reduction entry point on every Llama-3-8B
+    projection shape, q=4 g=32, sampled rows; both the signed and the Q*_1 layout."""
+    wl = synth.llama3_8b_decode()
+    for name, spec in wl.layers.items():
+        w = weights_host(spec)
+        x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
+        for mode in (O.SIGNED_SYM, O.ASYM_MIN):
+            check_matmul(w, x, 32, 4, mode, rows_idx=sample_rows(spec.rows, n=24, seed=M),
+                         tag=f"8b {name} M={M}", workspace=True, repeat=2, need_split=False)
 
 
 @pytest.mark.parametrize("M,workspace", [(1, False), (16, False), (16, True)])

@@ -56,7 +56,8 @@ def test_noalloc_matches_workspace_entry_point_over_consecutive_calls():
         assert torch.equal(y.t.view(torch.int16), y_ws.view(torch.int16)), f"{tag}: differs from ssq_matmul_ws"
         rows = sample_rows(N, n=24, seed=seed) if N > 64 else np.arange(N)
         ref_q = O.quantize(widen(w[rows], True), group, q, mode)
-        compare_matmul(y.t, widen(x_host, True), ref_q, rows, K, group, q, True, tag)
+        # the static scratch serves as the split workspace: the same kernel as ssq_matmul_ws
+        compare_matmul(y.t, widen(x_host, True), ref_q, rows, K, group, q, True, tag, workspace=True)
 
 
 def test_noalloc_inside_a_graph():
