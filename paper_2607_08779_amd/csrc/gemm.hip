@@ -49,6 +49,11 @@ struct Cfg {
   static constexpr int BM = 128 * WM;                   // output rows per workgroup tile
   static constexpr int kGroupWaves = 2 * WM;            // wavefronts per K-group
   static constexpr int kWaves = 2 * kGroupWaves;
+  // A wavefront covers all BM rows of the tile and BN / kGroupWaves columns: TI x TC
+  // MFMA tiles of 32 x 32, 128 accumulators per lane either way.
+  static constexpr int TI = BM / 32;
+  static constexpr int TC = BN / (32 * kGroupWaves);
+  static_assert(TI * TC == 8, "128 fp32 accumulators per lane");
   static constexpr int kThreads = 64 * kWaves;
   static constexpr int kStageBytes = BM * 128;          // BM rows x 64 bf16
   static constexpr int kLds = kStages * kStageBytes;    // 128 KB (WM = 2) or 64 KB (WM = 1)
@@ -67,12 +72,16 @@ __device__ __forceinline__ uint32_t swz(int r, int c) { return (uint32_t)(r * 12
 
 // 8 weights s*(u - o) of slice j (weights 8j..8j+7) of a 32-weight block held in q
 // dwords, natural order, as four bf16 pairs.  Each q-bit field is OR-ed into the
-// mantissa of the fp16 constant 1024 (0x6400 | u == 1024 + u), two fields per
-// instruction; one v_fma_mix_f32 per weight forms (1024 + u)*s + so with
-// so = -(1024 + o)*s (or m - 1024 s), both products exact in fp32, so the weight is
-// s*(u - o) exactly; it is rounded to bf16 once.
+// mantissa of the fp16 constant 1024, two fields per instruction, either where it
+// lies (bits 0..q-1 of a half: 0x6400 | u == 1024 + u) or one field higher without a
+// shift (bits q..2q-1: 0x6400 | (u << q) == 1024 + 2^q u, still inside the 10-bit
+// mantissa).  One v_fma_mix_f32 per weight then forms (1024 + u)*s + so[0], or
+// (1024 + 2^q u)*(s 2^-q) + so[1], with so[0] = -(1024 + o)*s and
+// so[1] = -(1024 2^-q + o)*s (or m - 1024 s, m - 1024 2^-q s): every product is exact
+// in fp32, so the weight is s*(u - o) exactly, rounded to bf16 once.  sc = {s, s 2^-q}.
 template <int Q>
-__device__ __forceinline__ bf16x8 dequant_slice(const uint32_t (&d)[Q], int j, float s, float so) {
+__device__ __forceinline__ bf16x8 dequant_slice(const uint32_t (&d)[Q], int j, const float (&sc)[2],
+                                                const float (&so)[2]) {
   const uint32_t magic = 0x64006400u;
   uint32_t sp;          // fields 0..3 of the slice at bit 0, fields 4..7 at bit 16
   if constexpr (Q == 4) {
@@ -88,87 +97,115 @@ __device__ __forceinline__ bf16x8 dequant_slice(const uint32_t (&d)[Q], int j, f
                               : d[2] >> 8;
     sp = (w & 0xFFFu) | ((w << 4) & 0x0FFF0000u);
   }
+  constexpr uint32_t kLow = Q == 4 ? 0x000F000Fu : Q == 3 ? 0x00070007u : 0x00030003u;
+  const uint32_t t = sp >> (2 * Q);           // fields 2, 3 (and 6, 7) at the bottom
+  const uint32_t p[4] = {and_or(sp, kLow, magic), and_or(sp, kLow << Q, magic), and_or(t, kLow, magic),
+                         and_or(t, kLow << Q, magic)};
   float f[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t p = and_or(sp >> (Q * i), Q == 4 ? 0x000F000Fu : Q == 3 ? 0x00070007u : 0x00030003u, magic);
-    f[i] = __builtin_fmaf(f16_lo(p), s, so);
-    f[i + 4] = __builtin_fmaf(f16_hi(p), s, so);
+  for (int i = 0; i < 4; ++i) {               // p[i] holds fields i and i + 4
+    f[i] = __builtin_fmaf(f16_lo(p[i]), sc[i & 1], so[i & 1]);
+    f[i + 4] = __builtin_fmaf(f16_hi(p[i]), sc[i & 1], so[i & 1]);
   }
   const uint32_t w0 = pack_bf16x2(f[0], f[1]), w1 = pack_bf16x2(f[2], f[3]);
   const uint32_t w2 = pack_bf16x2(f[4], f[5]), w3 = pack_bf16x2(f[6], f[7]);
   return __builtin_bit_cast(bf16x8, u32x4{w0, w1, w2, w3});
 }
 
-// Codes of one 32-weight block (4q bytes) through a buffer descriptor.
-template <int Q>
-__device__ __forceinline__ void load_block(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t (&d)[Q]) {
-  if constexpr (Q == 4) {
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
-    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-  } else if constexpr (Q == 3) {
-    const u32x3 v = __builtin_amdgcn_raw_buffer_load_b96(r, (int)off, 0, 0);
-    d[0] = v.x; d[1] = v.y; d[2] = v.z;
+// Constant term so[1] of dequant_slice for the fields OR-ed in one field higher:
+// -(1024 2^-q + o)*s (exact: an 11-bit integer by an 11-bit scale) or, for the binary16
+// minimum layout, m - 1024 2^-q s (one rounding).
+template <int META, int Q>
+__device__ __forceinline__ float dequant_offset_high(float s, uint32_t meta_bits) {
+  constexpr float kBase = (float)(1024 >> Q);
+  if constexpr (META == kMetaMin) {
+    return __builtin_fmaf(-kBase, s, f16_bits_to_f32(meta_bits));
   } else {
-    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
-    d[0] = v.x; d[1] = v.y;
+    const float o = META == kMetaZp ? (float)meta_bits : (float)(1 << (Q - 1));
+    return -(kBase + o) * s;
   }
 }
 
 // Work order.  Workgroups are dealt round-robin to the 8 XCDs (blockIdx % 8), each with
-// its own L2; when the work items divide evenly, XCD x takes a contiguous run of them.
-// Without a split the items are output tiles with the M tiles of one weight panel
-// together (a panel's codes are fetched once per XCD); with a split the K slices of a
-// tile come first, then the N tiles of one M tile (an XCD holds one activation panel
-// against a run of weight panels, and the slices of a tile meet on one XCD).
-__device__ __forceinline__ void work_item(int b, int tiles_m, int tiles_n, int splits, int& tm, int& tn,
-                                          int& split) {
-  const int items = tiles_m * tiles_n * splits;
+// its own L2; when a run of work items divides evenly, XCD x takes a contiguous part of
+// it.  Items are `full` whole output tiles, then the remaining tiles cut into `splits`
+// K slices each (all tiles are cut when full = 0, none when splits = 1).  Whole tiles
+// keep the M tiles of one weight panel together (a panel's codes are fetched once per
+// XCD); when every tile is cut, the K slices of a tile come first, then the N tiles of
+// one M tile (an XCD holds one activation panel against a run of weight panels).  The
+// slices of a tile are adjacent, so they meet on one XCD.  `cut` is the tile's index
+// among the cut tiles (its counter and partials), -1 for a whole tile.
+__device__ __forceinline__ void work_item(int b, int tiles_m, int tiles_n, int full, int splits, int& tm,
+                                          int& tn, int& split, int& cut) {
+  if (b < full) {
+    if (full % 8 == 0) b = (b % 8) * (full / 8) + b / 8;
+    split = 0;
+    cut = -1;
+    tm = b % tiles_m;
+    tn = b / tiles_m;
+    return;
+  }
+  b -= full;
+  const int items = (tiles_m * tiles_n - full) * splits;
   if (items % 8 == 0) b = (b % 8) * (items / 8) + b / 8;
-  const bool n_inner = splits > 1;
-  const int inner_count = n_inner ? tiles_n : tiles_m;
   split = b % splits;
-  const int rest = b / splits;
-  const int inner = rest % inner_count, outer = rest / inner_count;
-  tm = n_inner ? outer : inner;
-  tn = n_inner ? inner : outer;
+  cut = b / splits;
+  if (full == 0) {
+    tn = cut % tiles_n;
+    tm = cut / tiles_n;
+  } else {
+    tm = (full + cut) % tiles_m;
+    tn = (full + cut) / tiles_m;
+  }
 }
 
 // ---------------------------------------------------------------------------
 // Split reduction (host side).  When the output has too few tiles to give every CU a
-// workgroup, the K steps of each tile are divided among `splits` workgroups whose fp32
-// partial tiles meet in a caller-provided workspace: [counters: one u32 per tile, in the
-// fixed counter region][partials: tiles x splits x BM x BN fp32].
+// workgroup, or a last round of tiles would leave most CUs idle, the K steps of those
+// tiles are divided among `splits` workgroups whose fp32 partial tiles meet in a
+// caller-provided workspace: [counters: one u32 per cut tile, in the fixed counter
+// region][partials: cut tiles x splits x BM x BN fp32].  Without a workspace every tile
+// is computed whole.
 // ---------------------------------------------------------------------------
 constexpr int kMinStepsPerSplit = 16;
 
 struct Plan {
   int wm;            // wave tiles along M (tile height 128*wm)
   int64_t tiles;
+  int64_t full;      // tiles computed whole by one workgroup; the rest are cut into `splits`
   int splits;
   int64_t workspace; // bytes needed when splits > 1
 };
 
+// One workgroup per CU (WM = 2: 128 KB of LDS) or two (WM = 1): `slots` run at once.
+// Fewer tiles than slots: every tile is cut into K slices to fill them.  More: the tiles
+// run in rounds, and a last round less than half full is cut instead, so that its
+// slices fill the round and it takes a fraction of a round's time (896 tiles on 256
+// CUs: three rounds of whole tiles and one of 256 half tiles rather than a fourth round
+// of 128 tiles).
 Plan plan_for(int64_t M, int64_t N, int64_t K) {
   Plan p{};
   p.wm = M > 128 ? 2 : 1;
   const int64_t bm = 128 * p.wm;
   p.tiles = ((M + bm - 1) / bm) * ((N + BN - 1) / BN);
   const int64_t steps = (K / 32 + 1) / 2;
-  // one workgroup per CU (WM = 2: 128 KB of LDS) or two (WM = 1)
-  int64_t s = (p.wm == 2 ? 256 : 512) / p.tiles;
+  const int64_t slots = p.wm == 2 ? 256 : 512;
+  const int64_t last = p.tiles % slots;
+  const int64_t cut = p.tiles < slots ? p.tiles : (last != 0 && 2 * last <= slots ? last : 0);
+  int64_t s = cut > 0 ? slots / cut : 1;
   s = std::min<int64_t>(s, steps / kMinStepsPerSplit);
   s = std::min<int64_t>(s, 8);
-  if (p.tiles > kMaxSplitCounters) s = 1;
+  if (cut > kMaxSplitCounters) s = 1;
   p.splits = (int)std::max<int64_t>(s, 1);
-  p.workspace = p.splits > 1 ? kSplitCounterBytes + p.tiles * p.splits * bm * BN * 4 : 0;
+  p.full = p.splits > 1 ? p.tiles - cut : p.tiles;
+  p.workspace = p.splits > 1 ? kSplitCounterBytes + cut * p.splits * bm * BN * 4 : 0;
   return p;
 }
 
 template <int Q, int G, int META, int WM>
 __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
-    const void* __restrict__ meta, int M, int N, int K, int splits, uint16_t* __restrict__ y,
+    const void* __restrict__ meta, int M, int N, int K, int full, int splits, uint16_t* __restrict__ y,
     float* __restrict__ partials, unsigned int* __restrict__ counters) {
   using C = Cfg<WM>;
   constexpr int BM = C::BM;
@@ -192,18 +229,18 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar offsets
   const int grp = wave / C::kGroupWaves;                       // K-group: steps of parity grp
-  const int wp = wave % C::kGroupWaves;
-  const int wm = wp >> 1, wn = wp & 1;
+  const int wp = wave % C::kGroupWaves;                        // column block of the wavefront
+  constexpr int TI = C::TI, TC = C::TC;
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  int tm, tn, split;
-  work_item((int)blockIdx.x, tiles_m, tiles_n, splits, tm, tn, split);
-  const int tile_id = tm * tiles_n + tn;
+  int tm, tn, split, cut;
+  work_item((int)blockIdx.x, tiles_m, tiles_n, full, splits, tm, tn, split, cut);
+  const int parts = cut >= 0 ? splits : 1;     // K slices of this workgroup's tile
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int nblk = K / 32;
   const int total_steps = (nblk + 1) / 2;
   // This workgroup's slice of the reduction: steps [s_begin, s_begin + nsteps), in
   // windows of two (the last window's odd step may lie past the slice: it reads zeros).
-  const int per_split = (total_steps + splits - 1) / splits;
+  const int per_split = (total_steps + parts - 1) / parts;
   const int s_begin = split * per_split;
   const int nsteps = total_steps - s_begin < per_split ? total_steps - s_begin : per_split;
   const int nwin = (nsteps + 1) / 2;
@@ -215,8 +252,7 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
 
   // Activation buffer descriptor relative to the tile's first row; rows past M read zeros.
   const uint32_t rows_a = (uint32_t)(M - m0 < BM ? M - m0 : BM);
-  const int64_t nw0 = n0 + wn * 64;
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(x + m0 * K, rows_a * (uint32_t)K * 2);
+  const int64_t nw0 = n0 + wp * 32 * TC;
 
   // Activation staging: thread t loads 8 chunks of 16 bytes of stage e = t / (threads/2)
   // of the next window, rows 8 at a time: load i of wavefront v fills rows 8 (8 v' + i) ..
@@ -230,15 +266,22 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   const int a_c0 = (lane & 7) ^ (lane >> 4), a_c1 = a_c0 ^ 4;
   const uint32_t a_row = (uint32_t)(64 * a_w + (lane >> 3)) * (uint32_t)K * 2;
   const uint32_t a_b0 = a_row + a_c0 * 16, a_b1 = a_row + a_c1 * 16;
+  uint32_t a_off[8];                     // per-lane offsets, the same in every window
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a_off[i] = ((i & 1) ? a_b1 : a_b0) + (uint32_t)i * 16u * (uint32_t)K;
+  const int a_bytes = (int)(rows_a * (uint32_t)K * 2);
   auto issue_a = [&](int win, auto pair_c) {
     constexpr int pair = decltype(pair_c)::value;
-    const uint32_t col = (uint32_t)(s_begin + 2 * win + a_e) * 128u;
+    // The window's k offset moves the descriptor (scalar arithmetic) rather than every
+    // lane's offset; its size shrinks by as much, so the range check is unchanged.
+    const int col = (s_begin + 2 * win + a_e) * 128;
+    const int rest = a_bytes - col > 0 ? a_bytes - col : 0;
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(x + m0 * K + col / 2, (uint32_t)rest);
     auto fill = [&](uint8_t* st) {
 #pragma unroll
       for (int i = 0; i < 8; ++i)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(
-            ra, (__attribute__((address_space(3))) void*)(st + a_w * 8192 + i * 1024), 16,
-            ((i & 1) ? a_b1 : a_b0) + ((uint32_t)i * 16u * (uint32_t)K + col), 0, 0, 0);
+            rw, (__attribute__((address_space(3))) void*)(st + a_w * 8192 + i * 1024), 16, a_off[i], 0, 0, 0);
     };
     if (a_e == 0) fill(stage(std::integral_constant<int, 2 * pair>{}));
     else fill(stage(std::integral_constant<int, 2 * pair + 1>{}));
@@ -320,11 +363,11 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   const int h = lane >> 5, lr = lane & 31;
   const int kblk = 2 * grp + h;                  // the lane's block within a window (0..3)
 
-  f32x16 acc[4][2];
+  f32x16 acc[TI][TC];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < TC; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][c][r] = 0.0f;
 
@@ -334,14 +377,16 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     const uint8_t* bs = bstage(pair_c, 1);
     const uint8_t* bm = bstage(pair_c, 2);
     const uint32_t blk = 2u * (uint32_t)(s_begin + 2 * win) + (uint32_t)kblk;
-    // a block past the slice or past K weighs zero: scale and metadata forced to 0
+    // a block past the slice or past K weighs zero: scale and metadata forced to 0 (the
+    // reads themselves stay inside the row's 16 bytes of the stage, so they are always
+    // made and their results selected)
     const bool valid = (2 * win + grp < nsteps) & (blk < (uint32_t)nblk);
     const uint32_t g0 = (2u * (uint32_t)(s_begin + 2 * win)) / (G / 32), gi = blk / (G / 32);
-    uint32_t cw[2][Q];
-    float s[2], so[2];
+    uint32_t cw[TC][Q];
+    float sc[TC][2], so[TC][2];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int row = wn * 64 + 32 * c + lr;
+    for (int c = 0; c < TC; ++c) {
+      const int row = wp * 32 * TC + 32 * c + lr;
       if constexpr (Q == 4) {
         const u32x4 v = *reinterpret_cast<const u32x4*>(bc + (row * 4 + (kblk ^ ((row >> 2) & 3))) * 16);
         cw[c][0] = v.x; cw[c][1] = v.y; cw[c][2] = v.z; cw[c][3] = v.w;
@@ -354,7 +399,8 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
       }
       const uint32_t rbase = (uint32_t)row * groups_per_row;
       const uint32_t s_in = s_shift + (rbase + gi) * 2u - ((s_shift + (rbase + g0) * 2u) & ~3u);
-      const uint32_t sbits = valid ? (uint32_t)*reinterpret_cast<const uint16_t*>(bs + row * 16 + s_in) : 0u;
+      const uint32_t sraw = *reinterpret_cast<const uint16_t*>(bs + row * 16 + s_in);
+      const uint32_t sbits = valid ? sraw : 0u;
       uint32_t mbits = 0u;
       if constexpr (ZP) {
         const uint32_t m_in = m_shift + (rbase + gi) * kMetaSize - ((m_shift + (rbase + g0) * kMetaSize) & ~3u);
@@ -362,23 +408,42 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
                                               : (uint32_t)bm[row * 16 + m_in];
         mbits = valid ? raw : 0u;
       }
-      s[c] = f16_bits_to_f32(sbits);
-      so[c] = dequant_offset<META, Q>(s[c], mbits);
+      const float s = f16_bits_to_f32(sbits);
+      sc[c][0] = s;
+      sc[c][1] = s * (1.0f / (float)(1 << Q));
+      so[c][0] = dequant_offset<META, Q>(s, mbits);
+      so[c][1] = dequant_offset_high<META, Q>(s, mbits);
     }
+    // Operand reads run one slice ahead: slice j+1's activation fragments are requested
+    // before slice j's weights are dequantized and its MFMAs issued, so the LDS latency
+    // hides behind that work.
+    bf16x8 a[2][TI];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      bf16x8 a[4], b[2];
+    for (int i = 0; i < TI; ++i) a[0][i] = *reinterpret_cast<const bf16x8*>(at + swz(i * 32 + lr, 4 * h));
+    // Scheduling fences keep each group of reads at the head of the previous slice.
+    __builtin_amdgcn_sched_barrier(0);
+    auto slice = [&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      if constexpr (j < 3) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(at + swz(wm * 128 + i * 32 + lr, 4 * h + j));
+        for (int i = 0; i < TI; ++i)
+          a[(j + 1) & 1][i] = *reinterpret_cast<const bf16x8*>(at + swz(i * 32 + lr, 4 * h + j + 1));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      bf16x8 b[TC];
 #pragma unroll
-      for (int c = 0; c < 2; ++c) b[c] = dequant_slice<Q>(cw[c], j, s[c], so[c]);
+      for (int c = 0; c < TC; ++c) b[c] = dequant_slice<Q>(cw[c], j, sc[c], so[c]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
-          acc[i][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[c], acc[i][c], 0, 0, 0);
-    }
+        for (int c = 0; c < TC; ++c)
+          acc[i][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[j & 1][i], b[c], acc[i][c], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    slice(std::integral_constant<int, 0>{});
+    slice(std::integral_constant<int, 1>{});
+    slice(std::integral_constant<int, 2>{});
+    slice(std::integral_constant<int, 3>{});
   };
 
   // Window t: issue the loads of window t+1 (activations and weight stage, straight into
@@ -409,101 +474,102 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   wait_vmcnt<0>();     // the last window's (empty) loads, before LDS is reused
   __syncthreads();
 
-  // The K-groups meet: group g keeps M tiles 2g and 2g+1 of its wave tile and hands the
-  // other two to its partner (the same wave position in the other group) through LDS;
-  // the activation ring is idle after the last barrier.  Layout: 16 KB per wavefront,
-  // lane-contiguous 16-byte pieces (conflict-free).  The kept and given tiles are named
-  // with compile-time indices (grp is uniform per wavefront, so the branch is too): a
-  // runtime index would move the accumulators to scratch memory.
-  f32x16 own[2][2];
+  // The K-groups meet: group g keeps M tiles [g TI/2, (g+1) TI/2) of its wave tile and
+  // hands the other half to its partner (the same wave position in the other group)
+  // through LDS; the activation ring is idle after the last barrier.  Layout: 16 KB per
+  // wavefront, lane-contiguous 16-byte pieces (conflict-free).  The kept and given tiles
+  // are named with compile-time indices (grp is uniform per wavefront, so the branch is
+  // too): a runtime index would move the accumulators to scratch memory.
+  constexpr int TH = TI / 2;
+  f32x16 own[TH][TC];
   auto exchange = [&](auto keep_c) {
-    constexpr int keep = decltype(keep_c)::value, give = 2 - keep;
+    constexpr int keep = decltype(keep_c)::value, give = TH - keep;
     constexpr int kPerStage = C::kStageBytes / 16384;     // wavefront areas per stage
     float* xo = reinterpret_cast<float*>(stage_dyn(wave / kPerStage)) + (size_t)(wave % kPerStage) * 4096;
 #pragma unroll
-    for (int ii = 0; ii < 2; ++ii)
+    for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < TC; ++c)
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
           const f32x4 v = {acc[give + ii][c][4 * q4], acc[give + ii][c][4 * q4 + 1], acc[give + ii][c][4 * q4 + 2],
                            acc[give + ii][c][4 * q4 + 3]};
-          *reinterpret_cast<f32x4*>(xo + ((ii * 2 + c) * 4 + q4) * 256 + lane * 4) = v;
+          *reinterpret_cast<f32x4*>(xo + ((ii * TC + c) * 4 + q4) * 256 + lane * 4) = v;
         }
 #pragma unroll
-    for (int ii = 0; ii < 2; ++ii)
+    for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-      for (int c = 0; c < 2; ++c) own[ii][c] = acc[keep + ii][c];
+      for (int c = 0; c < TC; ++c) own[ii][c] = acc[keep + ii][c];
   };
   if (grp == 0) exchange(std::integral_constant<int, 0>{});
-  else exchange(std::integral_constant<int, 2>{});
+  else exchange(std::integral_constant<int, TH>{});
   __syncthreads();
   {
     constexpr int kPerStage = C::kStageBytes / 16384;
     const int partner = (1 - grp) * C::kGroupWaves + wp;
     const float* xi = reinterpret_cast<const float*>(stage_dyn(partner / kPerStage)) + (size_t)(partner % kPerStage) * 4096;
 #pragma unroll
-    for (int ii = 0; ii < 2; ++ii)
+    for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < TC; ++c)
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
-          const f32x4 v = *reinterpret_cast<const f32x4*>(xi + ((ii * 2 + c) * 4 + q4) * 256 + lane * 4);
+          const f32x4 v = *reinterpret_cast<const f32x4*>(xi + ((ii * TC + c) * 4 + q4) * 256 + lane * 4);
 #pragma unroll
           for (int e = 0; e < 4; ++e) own[ii][c][4 * q4 + e] += v[e];
         }
   }
-  const int keep = 2 * grp;     // M tiles keep, keep+1 of the wave tile are this wavefront's
+  const int keep = TH * grp;    // M tiles keep .. keep + TH - 1 of the wave tile are this wavefront's
 
-  if (splits > 1) {
+  if (cut >= 0) {
     // Split reduction: publish this slice's partial (the 64 accumulators this wavefront
     // owns, in lane order: coalesced), then count arrivals; the last arriving workgroup
     // sums all slices in slice order, writes y and resets the counter so the workspace
     // stays reusable.  Partials are written and read with device-scope (sc1) accesses,
     // which go to memory rather than this XCD's L2, so no device-wide fence is needed:
     // a store's vmcnt is released once memory has acknowledged it.
-    float* mine = partials + ((int64_t)tile_id * splits + split) * (BM * BN) + (int64_t)wave * 4096 + lane;
+    float* mine = partials + ((int64_t)cut * splits + split) * (BM * BN) + (int64_t)wave * 4096 + lane;
 #pragma unroll
-    for (int ii = 0; ii < 2; ++ii)
+    for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < TC; ++c)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          __hip_atomic_store(mine + ((ii * 2 + c) * 16 + r) * 64, own[ii][c][r], __ATOMIC_RELAXED,
+          __hip_atomic_store(mine + ((ii * TC + c) * 16 + r) * 64, own[ii][c][r], __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
     wait_vmcnt<0>();                       // every partial store acknowledged by memory
     unsigned int* arrived = reinterpret_cast<unsigned int*>(st0);
     __syncthreads();                       // the exchange above has finished reading LDS
-    if (tid == 0) *arrived = atomicAdd(&counters[tile_id], 1u);
+    if (tid == 0) *arrived = atomicAdd(&counters[cut], 1u);
     __syncthreads();
     if (*arrived != (unsigned int)(splits - 1)) return;   // uniform across the workgroup
 #pragma unroll
-    for (int ii = 0; ii < 2; ++ii)
+    for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int c = 0; c < TC; ++c)
 #pragma unroll
         for (int r = 0; r < 16; ++r) own[ii][c][r] = 0.0f;
     for (int o = 0; o < splits; ++o) {
-      const float* part_o = partials + ((int64_t)tile_id * splits + o) * (BM * BN) + (int64_t)wave * 4096 + lane;
+      const float* part_o = partials + ((int64_t)cut * splits + o) * (BM * BN) + (int64_t)wave * 4096 + lane;
 #pragma unroll
-      for (int ii = 0; ii < 2; ++ii)
+      for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+        for (int c = 0; c < TC; ++c)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            own[ii][c][r] += __hip_atomic_load(part_o + ((ii * 2 + c) * 16 + r) * 64, __ATOMIC_RELAXED,
+            own[ii][c][r] += __hip_atomic_load(part_o + ((ii * TC + c) * 16 + r) * 64, __ATOMIC_RELAXED,
                                                __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (tid == 0) __hip_atomic_store(&counters[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(&counters[cut], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
 #pragma unroll
-  for (int ii = 0; ii < 2; ++ii)
+  for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < TC; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + wm * 128 + (keep + ii) * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        const int64_t m = m0 + (keep + ii) * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
         const int64_t n = nw0 + c * 32 + lr;
         if (m < M && n < N) y[m * N + n] = f32_to_bf16_bits(own[ii][c][r]);
       }
@@ -516,16 +582,17 @@ hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, con
   const Plan p = plan_for(M, N, K);
   const bool split = p.splits > 1 && workspace != nullptr && (int64_t)workspace_bytes >= p.workspace;
   const int splits = split ? p.splits : 1;
+  const int64_t full = split ? p.full : p.tiles;
   unsigned int* counters = static_cast<unsigned int*>(workspace);
   float* partials = split ? reinterpret_cast<float*>(static_cast<char*>(workspace) + kSplitCounterBytes)
                           : nullptr;
-  const dim3 grid((unsigned)(p.tiles * splits));
+  const dim3 grid((unsigned)(full + (p.tiles - full) * splits));
   if (p.wm == 2)
     gemm_kernel<Q, G, META, 2><<<grid, Cfg<2>::kThreads, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N,
-                                                                   (int)K, splits, y, partials, counters);
+                                                                   (int)K, (int)full, splits, y, partials, counters);
   else
     gemm_kernel<Q, G, META, 1><<<grid, Cfg<1>::kThreads, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N,
-                                                                   (int)K, splits, y, partials, counters);
+                                                                   (int)K, (int)full, splits, y, partials, counters);
   return hipGetLastError();
 }
 

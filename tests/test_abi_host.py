@@ -105,7 +105,13 @@ def test_workspace_size_rules():
     # M=512 x N=4096 has 64 output tiles of 256x128, too few for 256 CUs: split 4 ways
     n = lib.ssq_matmul_workspace_size(512, 4096, 14336, 32, 4)
     assert n == COUNTERS + 64 * 4 * 256 * 128 * 4      # fixed counter region + partials
-    assert lib.ssq_matmul_workspace_size(2048, 14336, 4096, 32, 4) == 0   # enough tiles
+    assert lib.ssq_matmul_workspace_size(2048, 4096, 14336, 32, 4) == 0   # one full round of 256 tiles
+    assert lib.ssq_matmul_workspace_size(2048, 12288, 4096, 32, 4) == 0   # three full rounds
+    # 896 tiles: three rounds, then the last 128 tiles cut in two K slices
+    assert lib.ssq_matmul_workspace_size(2048, 14336, 4096, 32, 4) == COUNTERS + 128 * 2 * 256 * 128 * 4
+    # 1088 tiles: four rounds, then 64 tiles cut four ways
+    assert lib.ssq_matmul_workspace_size(2048, 17408, 5120, 32, 4) == COUNTERS + 64 * 4 * 256 * 128 * 4
+    assert lib.ssq_matmul_workspace_size(512, 28672, 8192, 32, 4) == 0    # last round 3/4 full: kept
     assert lib.ssq_matmul_workspace_size(1, 4096, 14336, 32, 4) == 0      # GEMV never splits
     # batched decode: 32 row blocks of 128 rows, 16 slices of K, one 16-token block
     assert lib.ssq_matmul_workspace_size(16, 4096, 14336, 32, 4) == COUNTERS + 32 * 16 * 8 * 256 * 4

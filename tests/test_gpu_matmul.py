@@ -253,6 +253,19 @@ def test_gemm_split_reduction_ragged(q, mode):
     check_matmul(w, x, 32, q, mode, tag="split 130x200x3104", workspace=True, repeat=3)
 
 
+@pytest.mark.parametrize("M,N,K", [(2048, 5120, 4096), (2000, 4700, 4096)])
+@pytest.mark.parametrize("mode", [O.SIGNED_SYM, O.ASYM_MIN])
+def test_gemm_split_last_round(M, N, K, mode):
+    # more output tiles than CUs (320, and a ragged 296) with a last round less than half
+    # full: those tiles (the weight panels from row 4096 on) are cut into K slices
+    # through the workspace while the others are computed whole
+    w = rand_w(N, K, seed=N + mode)
+    x = synth.activations(M, K, seed=M)
+    rows = np.concatenate([sample_rows(4096, n=8, seed=1), 4096 + sample_rows(N - 4096, n=40, seed=2)])
+    check_matmul(w, x, 32, 4, mode, rows_idx=rows, tag=f"split last round {M}x{N}x{K}", workspace=True,
+                 repeat=2)
+
+
 def test_gemm_split_reduction_eight_ways():
     w = rand_w(160, 8192, seed=5)
     x = synth.activations(64, 8192, seed=5)
@@ -445,6 +458,18 @@ def test_prefill_gemm_full_size(M, layer):
     x = synth.activations(M, spec.cols, seed=wl.x_seed + M)
     check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=sample_rows(spec.rows, n=32, seed=M),
                  tag=f"prefill {layer} M={M}")
+
+
+def test_prefill_gate_split_last_round_full_size():
+    """M=2048 on the 14336x4096 gate projection with a workspace: 896 tiles, the last 128
+    (rows 12288 on) cut in two K slices."""
+    wl = synth.prefill()
+    spec = wl.layers["gate_proj"]
+    w = weights_host(spec)
+    x = synth.activations(2048, spec.cols, seed=wl.x_seed + 2048)
+    rows = np.concatenate([sample_rows(12288, n=8, seed=3), 12288 + sample_rows(spec.rows - 12288, n=24, seed=4)])
+    check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=rows, tag="prefill gate_proj M=2048 split last round",
+                 workspace=True, repeat=2)
 
 
 def test_prefill_headline_split_full_size():
