@@ -126,23 +126,35 @@ __device__ __forceinline__ float dequant_offset_high(float s, uint32_t meta_bits
   }
 }
 
+// Tile t in the order whole tiles are taken: bands of `bh` M tiles (fewer in the last
+// band), each band swept along N with its M tiles together.  An XCD's run of tiles then
+// covers about bh activation panels and run/bh weight panels, each fetched into its L2
+// once while the workgroups sharing it run side by side; the host picks bh to make
+// that sum of panel bytes small.
+__device__ __forceinline__ void tile_at(int t, int tiles_m, int tiles_n, int bh, int& tm, int& tn) {
+  const int band = t / (bh * tiles_n);
+  const int h = tiles_m - bh * band < bh ? tiles_m - bh * band : bh;   // M tiles in this band
+  const int rem = t - bh * band * tiles_n;
+  tm = bh * band + rem % h;
+  tn = rem / h;
+}
+
 // Work order.  Workgroups are dealt round-robin to the 8 XCDs (blockIdx % 8), each with
 // its own L2; when a run of work items divides evenly, XCD x takes a contiguous part of
 // it.  Items are `full` whole output tiles, then the remaining tiles cut into `splits`
 // K slices each (all tiles are cut when full = 0, none when splits = 1).  Whole tiles
-// keep the M tiles of one weight panel together (a panel's codes are fetched once per
-// XCD); when every tile is cut, the K slices of a tile come first, then the N tiles of
-// one M tile (an XCD holds one activation panel against a run of weight panels).  The
-// slices of a tile are adjacent, so they meet on one XCD.  `cut` is the tile's index
-// among the cut tiles (its counter and partials), -1 for a whole tile.
-__device__ __forceinline__ void work_item(int b, int tiles_m, int tiles_n, int full, int splits, int& tm,
-                                          int& tn, int& split, int& cut) {
+// (and a cut last round) follow tile_at; when every tile is cut, the K slices of a tile
+// come first, then the N tiles of one M tile (an XCD holds one activation panel against
+// a run of weight panels).  The slices of a tile are adjacent, so they meet on one XCD.
+// `cut` is the tile's index among the cut tiles (its counter and partials), -1 for a
+// whole tile.
+__device__ __forceinline__ void work_item(int b, int tiles_m, int tiles_n, int full, int splits, int bh,
+                                          int& tm, int& tn, int& split, int& cut) {
   if (b < full) {
     if (full % 8 == 0) b = (b % 8) * (full / 8) + b / 8;
     split = 0;
     cut = -1;
-    tm = b % tiles_m;
-    tn = b / tiles_m;
+    tile_at(b, tiles_m, tiles_n, bh, tm, tn);
     return;
   }
   b -= full;
@@ -154,8 +166,7 @@ __device__ __forceinline__ void work_item(int b, int tiles_m, int tiles_n, int f
     tn = cut % tiles_n;
     tm = cut / tiles_n;
   } else {
-    tm = (full + cut) % tiles_m;
-    tn = (full + cut) / tiles_m;
+    tile_at(full + cut, tiles_m, tiles_n, bh, tm, tn);
   }
 }
 
@@ -202,10 +213,29 @@ Plan plan_for(int64_t M, int64_t N, int64_t K) {
   return p;
 }
 
+// Band height of the tile order: an XCD's run of whole tiles (a round's worth at most)
+// spans about bh activation panels of BM x K bf16 and run/bh weight panels of BN x K
+// codes with their scales and metadata; bh (a power of two up to the M tile count)
+// keeps the sum of those bytes smallest.
+int band_height(const Plan& p, int64_t M, int q, int group, int meta_bytes) {
+  const int64_t bm = 128 * p.wm;
+  const int64_t tiles_m = (M + bm - 1) / bm;
+  const int64_t run = std::max<int64_t>(1, std::min<int64_t>(p.tiles, p.wm == 2 ? 256 : 512) / 8);
+  const double a_panel = (double)bm * 2.0;
+  const double w_panel = (double)BN * ((double)q / 8.0 + (2.0 + meta_bytes) / group);
+  int bh = 1;
+  double best = a_panel + (double)run * w_panel;
+  for (int h = 2; h <= tiles_m; h *= 2) {
+    const double c = h * a_panel + (double)((run + h - 1) / h) * w_panel;
+    if (c < best) { best = c; bh = h; }
+  }
+  return bh;
+}
+
 template <int Q, int G, int META, int WM>
 __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     const uint16_t* __restrict__ x, const uint8_t* __restrict__ codes, const uint16_t* __restrict__ scales,
-    const void* __restrict__ meta, int M, int N, int K, int full, int splits, uint16_t* __restrict__ y,
+    const void* __restrict__ meta, int M, int N, int K, int full, int splits, int bh, uint16_t* __restrict__ y,
     float* __restrict__ partials, unsigned int* __restrict__ counters) {
   using C = Cfg<WM>;
   constexpr int BM = C::BM;
@@ -233,7 +263,7 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   constexpr int TI = C::TI, TC = C::TC;
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   int tm, tn, split, cut;
-  work_item((int)blockIdx.x, tiles_m, tiles_n, full, splits, tm, tn, split, cut);
+  work_item((int)blockIdx.x, tiles_m, tiles_n, full, splits, bh, tm, tn, split, cut);
   const int parts = cut >= 0 ? splits : 1;     // K slices of this workgroup's tile
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int nblk = K / 32;
@@ -587,12 +617,13 @@ hipError_t gemm_dispatch(const uint16_t* x, int64_t M, const uint8_t* codes, con
   float* partials = split ? reinterpret_cast<float*>(static_cast<char*>(workspace) + kSplitCounterBytes)
                           : nullptr;
   const dim3 grid((unsigned)(full + (p.tiles - full) * splits));
+  const int bh = band_height(p, M, Q, G, meta_size<META>());
   if (p.wm == 2)
     gemm_kernel<Q, G, META, 2><<<grid, Cfg<2>::kThreads, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N,
-                                                                   (int)K, (int)full, splits, y, partials, counters);
+                                                                   (int)K, (int)full, splits, bh, y, partials, counters);
   else
     gemm_kernel<Q, G, META, 1><<<grid, Cfg<1>::kThreads, 0, stream>>>(x, codes, scales, zp, (int)M, (int)N,
-                                                                   (int)K, (int)full, splits, y, partials, counters);
+                                                                   (int)K, (int)full, splits, bh, y, partials, counters);
   return hipGetLastError();
 }
 
