@@ -3,20 +3,21 @@
 // App. B.3 of the paper: What[n,k] = s[n,b] (u[n,k] - o[n,b]).  Prefill is a dense
 // contraction, so it runs on v_mfma_f32_32x32x16_bf16 with fp32 accumulation.
 //
-// Work split.  A wavefront owns a 128 (M) x 64 (N) output tile: 4 x 2 MFMA tiles of
-// 32 x 32, 128 fp32 accumulators per lane.  Only the activations and the packed weights
-// go through LDS; each wavefront dequantizes its own 64 weight rows straight into MFMA B
-// operands, so dequantized weights never cost LDS bandwidth.  A workgroup holds two
-// K-groups of 2*WM wavefronts (WM x 2 wave tiles: a (128*WM) x 128 output tile; WM = 2
-// unless M <= 128): K-group g
-// takes the 64-deep steps of parity g, so two wavefronts share each SIMD without
-// doubling the tile, and their accumulators meet in LDS at the end.  A "window" is one
-// step per K-group: its activation tiles (two stages) and its weight stage are read from
-// one half of their LDS rings while the next window's are loaded straight into the
-// other half (direct-to-LDS buffer loads, shared by the workgroup); one barrier per
-// window.  On gfx950 the matrix cores and the vector ALU of a SIMD do not run at the
-// same time (measured: an MFMA stream and a VALU stream take the sum of their times, in
-// one wavefront or in two), so the dequantization arithmetic adds to the MFMA time.
+// Work split.  A workgroup computes a (128*WM) x 128 output tile (WM = 2 unless
+// M <= 128) as two K-groups of 2*WM wavefronts: K-group g takes the 64-deep steps of
+// parity g, so two wavefronts share each SIMD without doubling the tile, and their
+// accumulators meet in LDS at the end.  Within a K-group a wavefront covers all 128*WM
+// rows and 128 / (2*WM) columns: TI x TC MFMA tiles of 32 x 32 (8 x 1 or 4 x 2), 128 fp32
+// accumulators per lane.  Only the activations and the packed weights go through LDS;
+// each wavefront dequantizes its own weight rows straight into MFMA B operands, so
+// dequantized weights never cost LDS bandwidth, and each dequantized operand feeds TI
+// MFMAs.  A "window" is one step per K-group: its activation tiles (two stages) and
+// its weight stage are read from one half of their LDS rings while the next window's
+// are loaded straight into the other half (direct-to-LDS buffer loads, shared by the
+// workgroup); one barrier per window.  On gfx950 the matrix cores and the vector ALU of
+// a SIMD do not run at the same time (measured: an MFMA stream and a VALU stream take
+// the sum of their times, in one wavefront or in two), so the dequantization arithmetic
+// adds to the MFMA time.
 //
 // Reduction order inside a step.  Lane l covers weight row l % 32 of an MFMA tile;
 // lanes 0-31 take the step's first 32-weight block, lanes 32-63 the second.  MFMA j
