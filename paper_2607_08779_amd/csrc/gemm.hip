@@ -554,42 +554,62 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
 
   if (cut >= 0) {
     // Split reduction: publish this slice's partial (the 64 accumulators this wavefront
-    // owns, in lane order: coalesced), then count arrivals; the last arriving workgroup
-    // sums all slices in slice order, writes y and resets the counter so the workspace
+    // owns, 16 bytes per lane per store, each store 1 KB contiguous), then count
+    // arrivals; the last arriving workgroup sums the slices in slice order (its own from
+    // registers, the others loaded), writes y and resets the counter so the workspace
     // stays reusable.  Partials are written and read with device-scope (sc1) accesses,
     // which go to memory rather than this XCD's L2, so no device-wide fence is needed:
     // a store's vmcnt is released once memory has acknowledged it.
-    float* mine = partials + ((int64_t)cut * splits + split) * (BM * BN) + (int64_t)wave * 4096 + lane;
+    constexpr int kSc1 = 16;                               // buffer aux bits: device-coherent
+    const __amdgpu_buffer_rsrc_t rp =
+        make_rsrc(partials + (int64_t)cut * splits * (BM * BN), (uint32_t)splits * (BM * BN) * 4u);
+    auto part_off = [&](int o, int ii, int c, int q4) {
+      return (uint32_t)((o * (BM * BN) + wave * 4096 + ((ii * TC + c) * 4 + q4) * 256 + lane * 4) * 4);
+    };
 #pragma unroll
     for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
       for (int c = 0; c < TC; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          __hip_atomic_store(mine + ((ii * TC + c) * 16 + r) * 64, own[ii][c][r], __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const f32x4 v = {own[ii][c][4 * q4], own[ii][c][4 * q4 + 1], own[ii][c][4 * q4 + 2], own[ii][c][4 * q4 + 3]};
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rp, (int)part_off(split, ii, c, q4), 0,
+                                                 kSc1);
+        }
     wait_vmcnt<0>();                       // every partial store acknowledged by memory
     unsigned int* arrived = reinterpret_cast<unsigned int*>(st0);
     __syncthreads();                       // the exchange above has finished reading LDS
     if (tid == 0) *arrived = atomicAdd(&counters[cut], 1u);
     __syncthreads();
     if (*arrived != (unsigned int)(splits - 1)) return;   // uniform across the workgroup
+    f32x16 mine[TH][TC];
 #pragma unroll
     for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
-      for (int c = 0; c < TC; ++c)
+      for (int c = 0; c < TC; ++c) {
+        mine[ii][c] = own[ii][c];
 #pragma unroll
         for (int r = 0; r < 16; ++r) own[ii][c][r] = 0.0f;
+      }
     for (int o = 0; o < splits; ++o) {
-      const float* part_o = partials + ((int64_t)cut * splits + o) * (BM * BN) + (int64_t)wave * 4096 + lane;
+      if (o == split) {                    // uniform: this workgroup's own slice
+#pragma unroll
+        for (int ii = 0; ii < TH; ++ii)
+#pragma unroll
+          for (int c = 0; c < TC; ++c) own[ii][c] += mine[ii][c];
+        continue;
+      }
 #pragma unroll
       for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
         for (int c = 0; c < TC; ++c)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            own[ii][c][r] += __hip_atomic_load(part_o + ((ii * TC + c) * 16 + r) * 64, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
+          for (int q4 = 0; q4 < 4; ++q4) {
+            const f32x4 v = __builtin_bit_cast(
+                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, (int)part_off(o, ii, c, q4), 0, kSc1));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) own[ii][c][4 * q4 + e] += v[e];
+          }
     }
     if (tid == 0) __hip_atomic_store(&counters[cut], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
