@@ -403,7 +403,7 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
       for (int r = 0; r < 16; ++r) acc[i][c][r] = 0.0f;
 
   // This K-group's step of window `win`: activation stage at `at`, weight stage `pair`.
-  auto compute = [&](const uint8_t* at, int win, auto pair_c) {
+  auto compute = [&](const uint8_t* at, int win, auto pair_c, auto&& issue_next) {
     const uint8_t* bc = bstage(pair_c, 0);
     const uint8_t* bs = bstage(pair_c, 1);
     const uint8_t* bm = bstage(pair_c, 2);
@@ -413,8 +413,10 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     // made and their results selected)
     const bool valid = (2 * win + grp < nsteps) & (blk < (uint32_t)nblk);
     const uint32_t g0 = (2u * (uint32_t)(s_begin + 2 * win)) / (G / 32), gi = blk / (G / 32);
-    uint32_t cw[TC][Q];
-    float sc[TC][2], so[TC][2];
+    // The step's LDS reads go out first (codes, scales, metadata, the first slice's
+    // activation fragments), then the next window's loads, and only then the arithmetic
+    // that waits for those reads: their latency hides behind the load issue.
+    uint32_t cw[TC][Q], sraw[TC], mraw[TC];
 #pragma unroll
     for (int c = 0; c < TC; ++c) {
       const int row = wp * 32 * TC + 32 * c + lr;
@@ -430,20 +432,13 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
       }
       const uint32_t rbase = (uint32_t)row * groups_per_row;
       const uint32_t s_in = s_shift + (rbase + gi) * 2u - ((s_shift + (rbase + g0) * 2u) & ~3u);
-      const uint32_t sraw = *reinterpret_cast<const uint16_t*>(bs + row * 16 + s_in);
-      const uint32_t sbits = valid ? sraw : 0u;
-      uint32_t mbits = 0u;
+      sraw[c] = *reinterpret_cast<const uint16_t*>(bs + row * 16 + s_in);
+      mraw[c] = 0u;
       if constexpr (ZP) {
         const uint32_t m_in = m_shift + (rbase + gi) * kMetaSize - ((m_shift + (rbase + g0) * kMetaSize) & ~3u);
-        const uint32_t raw = META == kMetaMin ? (uint32_t)*reinterpret_cast<const uint16_t*>(bm + row * 16 + m_in)
-                                              : (uint32_t)bm[row * 16 + m_in];
-        mbits = valid ? raw : 0u;
+        mraw[c] = META == kMetaMin ? (uint32_t)*reinterpret_cast<const uint16_t*>(bm + row * 16 + m_in)
+                                   : (uint32_t)bm[row * 16 + m_in];
       }
-      const float s = f16_bits_to_f32(sbits);
-      sc[c][0] = s;
-      sc[c][1] = s * (1.0f / (float)(1 << Q));
-      so[c][0] = dequant_offset<META, Q>(s, mbits);
-      so[c][1] = dequant_offset_high<META, Q>(s, mbits);
     }
     // Operand reads run one slice ahead: slice j+1's activation fragments are requested
     // before slice j's weights are dequantized and its MFMAs issued, so the LDS latency
@@ -451,6 +446,20 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     bf16x8 a[2][TI];
 #pragma unroll
     for (int i = 0; i < TI; ++i) a[0][i] = *reinterpret_cast<const bf16x8*>(at + swz(i * 32 + lr, 4 * h));
+    __builtin_amdgcn_sched_barrier(0);
+    issue_next();
+    __builtin_amdgcn_sched_barrier(0);
+    float sc[TC][2], so[TC][2];
+#pragma unroll
+    for (int c = 0; c < TC; ++c) {
+      const uint32_t sbits = valid ? sraw[c] : 0u;
+      const uint32_t mbits = valid ? mraw[c] : 0u;
+      const float s = f16_bits_to_f32(sbits);
+      sc[c][0] = s;
+      sc[c][1] = s * (1.0f / (float)(1 << Q));
+      so[c][0] = dequant_offset<META, Q>(s, mbits);
+      so[c][1] = dequant_offset_high<META, Q>(s, mbits);
+    }
     // Scheduling fences keep each group of reads at the head of the previous slice.
     __builtin_amdgcn_sched_barrier(0);
     auto slice = [&](auto jc) {
@@ -487,11 +496,12 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   __syncthreads();
   auto window = [&](int t, auto par) {
     constexpr int p = decltype(par)::value;
-    issue_a(t + 1, std::integral_constant<int, 1 - p>{});
-    issue_bstage(t + 1, std::integral_constant<int, 1 - p>{});
-    __builtin_amdgcn_sched_barrier(0);       // the loads go out before the arithmetic
+    // the next window's loads go out after this step's first LDS reads, before its arithmetic
     compute(grp == 0 ? stage(std::integral_constant<int, 2 * p>{}) : stage(std::integral_constant<int, 2 * p + 1>{}),
-            t, std::integral_constant<int, p>{});
+            t, std::integral_constant<int, p>{}, [&] {
+              issue_a(t + 1, std::integral_constant<int, 1 - p>{});
+              issue_bstage(t + 1, std::integral_constant<int, 1 - p>{});
+            });
     __builtin_amdgcn_sched_barrier(0);
     wait_vmcnt<0>();
     __syncthreads();
