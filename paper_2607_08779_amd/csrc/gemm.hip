@@ -43,6 +43,7 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int BN = 128;                  // output columns per workgroup tile
+constexpr uint32_t kOutOfRange = 0x80000000u;   // past every buffer a descriptor here covers
 constexpr int kStages = 4;               // activation ring: two windows of two steps
 
 template <int WM>
@@ -624,6 +625,27 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
     if (tid == 0) __hip_atomic_store(&counters[cut], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
+  // y: through a buffer descriptor when y, with M padded to whole tiles, spans under
+  // 1 GB (every offset then fits 32 bits, and so does an out-of-range base plus a row
+  // offset): a lane's column past N gets an offset past the buffer, a row past M lies
+  // past it anyway, so every store is issued and the range check drops those outside y.
+  if ((uint64_t)tiles_m * BM * (uint64_t)N * 2u < (1ull << 30)) {
+    const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, (uint32_t)M * (uint32_t)N * 2u);
+#pragma unroll
+    for (int ii = 0; ii < TH; ++ii)
+#pragma unroll
+      for (int c = 0; c < TC; ++c) {
+        const int64_t m = m0 + (keep + ii) * 32 + 4 * h;
+        const int64_t n = nw0 + c * 32 + lr;
+        const uint32_t base = n < N ? (uint32_t)((m * N + n) * 2) : kOutOfRange;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_bits(own[ii][c][r]), ry,
+                                                (int)(base + (uint32_t)(8 * (r >> 2) + (r & 3)) * (uint32_t)N * 2u),
+                                                0, 0);
+      }
+    return;
+  }
 #pragma unroll
   for (int ii = 0; ii < TH; ++ii)
 #pragma unroll
