@@ -243,6 +243,9 @@ SWEEP_MODES = ("signed_sym", "unsigned_sym", "asym", "asym_min")
 HBM_TARGET_BYTES = 600 << 20    # distinct weight bytes per timed pass: over twice the Infinity Cache
 
 
+WARMUP_S = 0.02   # GPU time spent before a sweep measurement's timed repetitions
+
+
 def _graph_time(torch, fn, reps: int) -> float:
     """Seconds per replay of a HIP graph holding the launches fn() makes."""
     s = torch.cuda.Stream()
@@ -256,9 +259,17 @@ def _graph_time(torch, fn, reps: int) -> float:
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=s):
             fn()
-        g.replay()
-        torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        g.replay()
+        e1.record(s)
+        torch.cuda.synchronize()
+        # Warm-up: replays for about WARMUP_S of GPU time first, so the timed replays run at
+        # the clock the load settles at (a cold start measured up to 15 % slower on the
+        # prefill GEMM).
+        for _ in range(min(1000, int(WARMUP_S / max(e0.elapsed_time(e1) / 1e3, 1e-6)))):
+            g.replay()
+        torch.cuda.synchronize()
         e0.record(s)
         for _ in range(reps):
             g.replay()
@@ -268,10 +279,16 @@ def _graph_time(torch, fn, reps: int) -> float:
 
 
 def _eager_time(torch, fn, reps: int) -> float:
-    """Seconds per call of fn() launched eagerly on the null stream (ssq_quantize's stream)."""
-    fn()
-    torch.cuda.synchronize()
+    """Seconds per call of fn() launched eagerly on the null stream (ssq_quantize's stream),
+    after about WARMUP_S of warm-up calls."""
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    fn()
+    e1.record()
+    torch.cuda.synchronize()
+    for _ in range(min(1000, int(WARMUP_S / max(e0.elapsed_time(e1) / 1e3, 1e-6)))):
+        fn()
+    torch.cuda.synchronize()
     e0.record()
     for _ in range(reps):
         fn()
