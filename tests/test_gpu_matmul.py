@@ -266,6 +266,16 @@ def test_gemm_split_last_round(M, N, K, mode):
                  repeat=2)
 
 
+def test_gemm_output_past_one_gigabyte():
+    """A 4096 x 131072 bf16 output (1 GiB): the GEMM stores it with 64-bit addresses rather
+    than through a buffer descriptor; sampled rows against the oracle, guards checked."""
+    N, K, M = 131072, 512, 4096
+    w = rand_w(N, K, seed=17)
+    x = synth.activations(M, K, seed=17)
+    rows = np.concatenate([sample_rows(N, n=24, seed=5), np.array([N - 129, N - 128, N - 127])])
+    check_matmul(w, x, 32, 4, O.SIGNED_SYM, rows_idx=np.unique(rows), tag="gemm 4096x131072x512 (1 GiB y)")
+
+
 def test_gemm_split_reduction_eight_ways():
     w = rand_w(160, 8192, seed=5)
     x = synth.activations(64, 8192, seed=5)
