@@ -629,6 +629,8 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   // 1 GB (every offset then fits 32 bits, and so does an out-of-range base plus a row
   // offset): a lane's column past N gets an offset past the buffer, a row past M lies
   // past it anyway, so every store is issued and the range check drops those outside y.
+  // The stores are non-temporal: this kernel never reads y, and the activation and
+  // weight panels other workgroups are reading keep their L2 lines.
   if ((uint64_t)tiles_m * BM * (uint64_t)N * 2u < (1ull << 30)) {
     const __amdgpu_buffer_rsrc_t ry = make_rsrc(y, (uint32_t)M * (uint32_t)N * 2u);
 #pragma unroll
@@ -642,7 +644,7 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
         for (int r = 0; r < 16; ++r)
           __builtin_amdgcn_raw_buffer_store_b16(f32_to_bf16_bits(own[ii][c][r]), ry,
                                                 (int)(base + (uint32_t)(8 * (r >> 2) + (r & 3)) * (uint32_t)N * 2u),
-                                                0, 0);
+                                                0, kStream);
       }
     return;
   }
