@@ -490,29 +490,56 @@ __global__ __launch_bounds__(Cfg<WM>::kThreads) void gemm_kernel(
   // Window t: issue the loads of window t+1 (activations and weight stage, straight into
   // the other half of each ring, last read in window t-1, before the previous barrier),
   // multiply this K-group's step of window t, wait for this thread's loads, barrier:
-  // every wavefront's part of window t+1's tiles is then in LDS.
+  // every wavefront's part of window t+1's tiles is then in LDS.  Without metadata,
+  // windows 0 and 1 are loaded together at the start, so window 1's loads are in flight
+  // from the first moment rather than after window 0 has landed; every wavefront issues
+  // window 1's 8 activation loads last, and loads complete in order, so at most 8
+  // outstanding means window 0 has landed (the barrier waits for LDS only: window 1
+  // stays in flight).  With metadata the extra live state of the peeled first window
+  // made the compiler spill around the main loop (measured 1.6 % slower), so those
+  // layouts start with window 0 alone.
+  constexpr bool kTwoWindowStart = !ZP;
   issue_a(0, std::integral_constant<int, 0>{});
   issue_bstage(0, std::integral_constant<int, 0>{});
-  wait_vmcnt<0>();
-  __syncthreads();
-  auto window = [&](int t, auto par) {
+  if constexpr (kTwoWindowStart) {
+    issue_bstage(1, std::integral_constant<int, 1>{});
+    issue_a(1, std::integral_constant<int, 1>{});
+    static_assert(C::kALoads == 8, "window 1's trailing activation loads");
+    wait_vmcnt<8>();
+    lds_barrier();
+  } else {
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+  auto window = [&](int t, auto par, auto issue_c) {
     constexpr int p = decltype(par)::value;
     // the next window's loads go out after this step's first LDS reads, before its arithmetic
     compute(grp == 0 ? stage(std::integral_constant<int, 2 * p>{}) : stage(std::integral_constant<int, 2 * p + 1>{}),
             t, std::integral_constant<int, p>{}, [&] {
-              issue_a(t + 1, std::integral_constant<int, 1 - p>{});
-              issue_bstage(t + 1, std::integral_constant<int, 1 - p>{});
+              if constexpr (decltype(issue_c)::value) {
+                issue_a(t + 1, std::integral_constant<int, 1 - p>{});
+                issue_bstage(t + 1, std::integral_constant<int, 1 - p>{});
+              }
             });
     __builtin_amdgcn_sched_barrier(0);
     wait_vmcnt<0>();
     __syncthreads();
   };
   int t = 0;
-  for (; t + 2 <= nwin; t += 2) {
-    window(t, std::integral_constant<int, 0>{});
-    window(t + 1, std::integral_constant<int, 1>{});
+  if constexpr (kTwoWindowStart) {
+    window(0, std::integral_constant<int, 0>{}, std::false_type{});
+    for (t = 1; t + 2 <= nwin; t += 2) {
+      window(t, std::integral_constant<int, 1>{}, std::true_type{});
+      window(t + 1, std::integral_constant<int, 0>{}, std::true_type{});
+    }
+    if (t < nwin) window(t, std::integral_constant<int, 1>{}, std::true_type{});
+  } else {
+    for (; t + 2 <= nwin; t += 2) {
+      window(t, std::integral_constant<int, 0>{}, std::true_type{});
+      window(t + 1, std::integral_constant<int, 1>{}, std::true_type{});
+    }
+    if (t < nwin) window(t, std::integral_constant<int, 0>{}, std::true_type{});
   }
-  if (t < nwin) window(t, std::integral_constant<int, 0>{});
   wait_vmcnt<0>();     // the last window's (empty) loads, before LDS is reused
   __syncthreads();
 

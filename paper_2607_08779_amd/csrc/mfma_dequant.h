@@ -136,4 +136,15 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | 0x70 | 0xF00 | ((N >> 4) << 14));
 }
 
+// Workgroup barrier for LDS only: this wavefront's LDS operations are waited for
+// (s_waitcnt lgkmcnt(0), the gfx9 encoding with vmcnt and expcnt at their maxima), then
+// s_barrier, written as a memory-clobbering asm statement.  The compiler's own barrier
+// (and __syncthreads' fences) also waits for every direct-to-LDS load in flight, i.e.
+// the prefetch, and for the global stores.  Callers make sure no LDS location read
+// after it is still being written by a load in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  asm volatile("s_barrier" ::: "memory");
+}
+
 }  // namespace ssq

@@ -429,17 +429,6 @@ struct StatLayout {
   static constexpr int kMetaWords = kMetaRow >= 4 ? kMetaRow / 4 : 1;
 };
 
-// Workgroup barrier for LDS only: this wavefront's LDS operations are waited for
-// (s_waitcnt lgkmcnt(0), the gfx9 encoding with vmcnt and expcnt at their maxima), then
-// s_barrier, written as a memory-clobbering asm statement.  The compiler's own barrier
-// (and __syncthreads' fences) also waits for every direct-to-LDS load in flight -- here
-// the next tiles' codes, i.e. the prefetch -- and for the global stores.  The LDS
-// accesses around it only touch the reduction area, which no load writes.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt(0xC07F);
-  asm volatile("s_barrier" ::: "memory");
-}
-
 // One row's `B` bytes of scales or metadata into dwords (B = 32, 16, 8, 4, 2 or 1; the
 // offset is a multiple of B, so every load is naturally aligned).
 template <int B>
@@ -776,8 +765,9 @@ __global__ __launch_bounds__(64 * kStatWaves) void skinny_stat_kernel(
 
   // Tiles in pairs (R is even): the loads of tile t+1 are in flight while tile t is
   // computed, and every pass issues the same loads and stores (so the compiler waits for
-  // the current tile's, not the next one's).  Barriers: after a tile's `part` is written
-  // (it is read by all), and after it is read (it is written again).
+  // the current tile's, not the next one's).  Barriers, for LDS only (no load writes
+  // `part`): after a tile's `part` is written (it is read by all), and after it is read
+  // (it is written again).
   f32x4 acc[MB];
   for (int t = 0; t < R; t += 2) {
     lds_barrier();
