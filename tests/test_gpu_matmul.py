@@ -236,6 +236,17 @@ def test_skinny_short_and_odd_reductions(K):
         check_matmul(w, x, 32, 3, mode, tag=f"skinny K={K}")
 
 
+@pytest.mark.parametrize("K", [32, 64, 96, 128, 192])
+@pytest.mark.parametrize("mode", [O.SIGNED_SYM, O.ASYM])
+def test_gemm_short_reductions(K, mode):
+    # one or two 64-deep windows per tile: the loads of the window after the last one
+    # (issued at the start of the tile, or by the last window) lie past K and read
+    # nothing the result uses; signed scales take the two-window start, zero points not
+    w = rand_w(300, K, seed=K + mode)
+    x = synth.activations(200, K, seed=K)
+    check_matmul(w, x, 32, 4, mode, tag=f"gemm 200x300x{K}")
+
+
 @pytest.mark.parametrize("M", [2, 3, 16, 32, 33, 129])
 def test_gemm_small_token_counts(M):
     w = rand_w(64, 512, seed=M)
